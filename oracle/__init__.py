@@ -1,0 +1,3 @@
+"""fp64 CPU oracle of the MoE layer (test infrastructure only; see moe_oracle)."""
+from .moe_oracle import (route, permute, swiglu_ffn, ffn_rows, combine, layer,  # noqa: F401
+                         dense_swiglu, token_outputs)
