@@ -1,0 +1,170 @@
+/*
+ * moe.h - C ABI of the MI355X (gfx950) MoE-layer hot path.
+ *
+ * One Mixture-of-Experts layer over an expert-level batch: the module the
+ * paper's forward pass (Algorithm 1) runs on the hidden states COMBINEd from
+ * many yielded sequences, h_out <- MoE(h, l).  The layer is the top-k
+ * softmax-gated SwiGLU expert layer of the Mixtral and DeepSeek models the
+ * paper evaluates (Section 6, Models); its motivation is sparse expert
+ * activation with uneven expert popularity (Section 2.2, Insight 1) and the
+ * large expert batch needed to saturate the GPU (Section 7, batch-size regime).
+ *
+ * Four calls, issued in order on one stream, make the layer:
+ *   moe_route        logits -> top-k expert ids and gate weights
+ *   moe_permute      ids, x -> per-expert counts, offsets, row maps, x_perm
+ *   moe_grouped_ffn  x_perm -> y_perm, each expert's SwiGLU FFN on its rows
+ *   moe_combine      y_perm -> y, gate-weighted sum of each token's k rows
+ * A shared (always active) expert is one more moe_grouped_ffn call with E = 1
+ * over x itself, whose output moe_combine adds with weight 1.
+ *
+ * Conventions (all calls)
+ *   - Every pointer argument is a DEVICE pointer unless stated otherwise, owned
+ *     by the caller.  The library never allocates, frees or synchronizes in
+ *     these calls: work is enqueued on `stream` (a hipStream_t; NULL is the
+ *     default stream) and the call returns.  Buffers must not overlap.
+ *   - Row-major layouts.  Shapes are given as [rows, cols].
+ *   - Every base pointer must be 16-byte aligned.
+ *   - Validation is done on the host before anything is enqueued.  On an error
+ *     nothing is written and nothing is launched; moe_last_error() then holds
+ *     a message naming the argument.  T = 0 (or R = 0) returns MOE_OK and
+ *     enqueues nothing; pointers may then be NULL.
+ *   - Not checked (preconditions): finite logits; expert ids in [0, E) and
+ *     distinct within a token (moe_route guarantees both); offsets consistent
+ *     with R; buffers large enough for the stated shapes.
+ *   - Device faults surface asynchronously at the caller's next synchronization.
+ *   - Thread-safe; calls on different streams are independent.
+ *   - Deterministic: identical inputs give bitwise-identical outputs (no atomics
+ *     decide any result).
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARGUMENT = 1,    /* null pointer, bad size, misalignment */
+    MOE_ERR_UNSUPPORTED = 2,         /* E > 256, k > 16, unknown dtype */
+    MOE_ERR_WORKSPACE_TOO_SMALL = 3,
+    MOE_ERR_HIP = 4                  /* a HIP runtime call or kernel launch failed */
+} moe_status;
+
+typedef enum {
+    MOE_DTYPE_F32 = 0,               /* fp32 activations and weights, fp32 arithmetic */
+    MOE_DTYPE_BF16 = 1               /* bf16 activations and weights, fp32 accumulation */
+} moe_dtype;
+
+typedef void* moe_stream;            /* hipStream_t */
+
+#define MOE_ABI_VERSION 1
+#define MOE_MAX_EXPERTS 256
+#define MOE_MAX_TOPK 16
+
+/* ABI version of the loaded library (MOE_ABI_VERSION). */
+int moe_abi_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* moe_status_string(int status);
+
+/* Message of the last failed call on this host thread ("" if none).  The
+ * pointer stays valid until the next call on the same thread. */
+const char* moe_last_error(void);
+
+/*
+ * moe_route - top-k gating (the MoE gate the expert batch reaches; the paper's
+ * Section 2.2 expert selection).
+ *
+ *   logits        f32 [T, E]   gating logits (the router GEMM is the caller's)
+ *   topk_ids      i32 [T, k]   out: slot 0 holds the largest logit
+ *   topk_weights  f32 [T, k]   out: gate weights
+ *
+ * Order: larger logit first; equal logits (including +0 and -0) go to the
+ * lower expert id.  Selection compares the fp32 logits exactly.  Weights:
+ * p_e = exp(l_e - l_max); renormalize = 1 gives p / sum over the k selected,
+ * renormalize = 0 gives p / sum over all E.  exp and the division are fp32.
+ * Errors: INVALID_ARGUMENT for T < 0, E < 1, k < 1, k > E, T*k > INT32_MAX,
+ * renormalize not 0/1, null or misaligned pointers; UNSUPPORTED for E > 256 or
+ * k > 16.
+ */
+moe_status moe_route(const float* logits, int64_t T, int32_t E, int32_t k, int32_t renormalize,
+                     int32_t* topk_ids, float* topk_weights, moe_stream stream);
+
+/*
+ * moe_permute - group the T*k (token, slot) assignments by expert and gather
+ * each assignment's hidden row (the expert-level batch built by COMBINE,
+ * Section 4.2 and Algorithm 1, regrouped per expert).
+ *
+ *   topk_ids          i32 [T, k]      expert of each assignment (from moe_route)
+ *   x                 dt  [T, H]      hidden states
+ *   expert_counts     i32 [E]         out: rows per expert
+ *   expert_offsets    i32 [E + 1]     out: exclusive prefix sum, offsets[E] = T*k
+ *   sorted_token_ids  i32 [T*k]       out: source token of each grouped row
+ *   dest_rows         i32 [T, k]      out: grouped row of assignment (t, j)
+ *   x_perm            dt  [T*k, H]    out: x_perm[r] = x[sorted_token_ids[r]]
+ *   ws, ws_bytes      device scratch of at least moe_permute_workspace_bytes()
+ *
+ * Expert e owns rows offsets[e] .. offsets[e+1]-1, holding its tokens in
+ * ascending token order (a stable counting sort).
+ * Errors: as moe_route, plus INVALID_ARGUMENT for H < 64 or H % 64 != 0,
+ * UNSUPPORTED for an unknown dtype, WORKSPACE_TOO_SMALL.
+ */
+size_t moe_permute_workspace_bytes(int64_t T, int32_t E, int32_t k);
+moe_status moe_permute(const int32_t* topk_ids, const void* x, int64_t T, int32_t E, int32_t k,
+                       int32_t H, moe_dtype dt, int32_t* expert_counts, int32_t* expert_offsets,
+                       int32_t* sorted_token_ids, int32_t* dest_rows, void* x_perm,
+                       void* ws, size_t ws_bytes, moe_stream stream);
+
+/*
+ * moe_grouped_ffn - every expert's SwiGLU FFN on its own rows, as one grouped
+ * GEMM pair (the expert computation of the MoE module in Algorithm 1).
+ *
+ *   x_perm          dt  [R, H]     rows grouped by expert
+ *   expert_offsets  i32 [E + 1]    DEVICE array; group e = rows offsets[e]..offsets[e+1]-1
+ *   w_gate, w_up    dt  [E, F, H]  K-contiguous (each row is one output feature)
+ *   w_down          dt  [E, H, F]  K-contiguous
+ *   y_perm          dt  [R, H]     out: W_down[e] (silu(W_gate[e] x) * (W_up[e] x))
+ *   ws, ws_bytes    device scratch of at least moe_grouped_ffn_workspace_bytes();
+ *                   it holds the intermediate h [R, F]
+ *
+ * silu(z) = z / (1 + exp(-z)).  bf16: fp32 accumulation, h and y_perm rounded
+ * to bf16 (nearest even).  f32: fp32 throughout.  Group sizes are read on the
+ * device only (no host readback).
+ * Errors: INVALID_ARGUMENT for R < 0, E < 1, H or F not a positive multiple of
+ * 64, R > INT32_MAX, null or misaligned pointers; UNSUPPORTED for E > 256 or
+ * an unknown dtype; WORKSPACE_TOO_SMALL.
+ */
+size_t moe_grouped_ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt);
+moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, int64_t R, int32_t E,
+                           int32_t H, int32_t F, const void* w_gate, const void* w_up,
+                           const void* w_down, moe_dtype dt, void* y_perm, void* ws,
+                           size_t ws_bytes, moe_stream stream);
+
+/*
+ * moe_combine - gate-weighted sum of each token's k expert outputs (the MoE
+ * module's output h_out in Algorithm 1).
+ *
+ *   y_perm        dt  [T*k, H]  expert outputs in grouped order
+ *   dest_rows     i32 [T, k]    grouped row of assignment (t, j) (from moe_permute)
+ *   topk_weights  f32 [T, k]
+ *   y_shared      dt  [T, H]    optional (NULL = none): added with weight 1
+ *   y             dt  [T, H]    out: sum_j w[t,j] * y_perm[dest_rows[t,j]] (+ y_shared[t])
+ *
+ * The sum is formed in fp32 in slot order j = 0..k-1, the shared row added
+ * last, then rounded once to dt.  Gather form: no atomics.
+ * Errors: INVALID_ARGUMENT for T < 0, k < 1, k > 16 (UNSUPPORTED), H not a
+ * positive multiple of 64, T*k > INT32_MAX, null or misaligned pointers.
+ */
+moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float* topk_weights,
+                       const void* y_shared, int64_t T, int32_t k, int32_t H, moe_dtype dt, void* y,
+                       moe_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

@@ -1,0 +1,237 @@
+"""Python binding of libmoe.so, the gfx950 MoE-layer hot path.
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  PyTorch supplies device memory and the stream; outputs that are not
+passed in are allocated with ``torch.empty`` on the input's device.
+
+The binding fails loudly when the library is missing: there is no CPU or
+PyTorch fallback for any call.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+__all__ = [
+    "MoEError", "lib", "LIB_PATH", "HEADER_PATH", "abi_version", "exported_symbols",
+    "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
+    "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
+    "DTYPE_F32", "DTYPE_BF16",
+]
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmoe.so")
+HEADER_PATH = os.path.join(os.path.dirname(HERE), "include", "moe.h")
+
+DTYPE_F32, DTYPE_BF16 = 0, 1
+_STATUS = {0: "MOE_OK", 1: "MOE_ERR_INVALID_ARGUMENT", 2: "MOE_ERR_UNSUPPORTED",
+           3: "MOE_ERR_WORKSPACE_TOO_SMALL", 4: "MOE_ERR_HIP"}
+
+
+class MoEError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "moe_abi_version": (ctypes.c_int, []),
+    "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "moe_last_error": (ctypes.c_char_p, []),
+    "moe_route": (ctypes.c_int, [_P, _I64, _I32, _I32, _I32, _P, _P, _P]),
+    "moe_permute_workspace_bytes": (_SZ, [_I64, _I32, _I32]),
+    "moe_permute": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P,
+                                   _P, _SZ, _P]),
+    "moe_grouped_ffn_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I32, ctypes.c_int]),
+    "moe_grouped_ffn": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, ctypes.c_int, _P,
+                                       _P, _SZ, _P]),
+    "moe_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I32, _I32, ctypes.c_int, _P, _P]),
+}
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -c 'import __graft_entry__ as g; g.build()'`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def exported_symbols():
+    """Function names declared in include/moe.h."""
+    text = open(HEADER_PATH).read()
+    return sorted(set(re.findall(r"^\s*(?:[\w\*]+\s+)+\**(moe_\w+)\s*\(", text, flags=re.M)))
+
+
+def abi_version() -> int:
+    return lib().moe_abi_version()
+
+
+def _check(status: int):
+    if status != 0:
+        msg = lib().moe_last_error().decode()
+        raise MoEError(status, msg)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("all tensors must be on the GPU")
+        if t is not None and not t.is_contiguous():
+            raise ValueError("all tensors must be contiguous")
+
+
+# --------------------------------------------------------------------------- the four calls
+def moe_route(logits, k, renormalize=1, topk_ids=None, topk_weights=None, stream=None):
+    """logits f32 [T, E] -> (topk_ids i32 [T, k], topk_weights f32 [T, k])."""
+    T, E = logits.shape
+    if logits.dtype != torch.float32:
+        raise TypeError("logits must be float32")
+    if topk_ids is None:
+        topk_ids = torch.empty((T, k), dtype=torch.int32, device=logits.device)
+    if topk_weights is None:
+        topk_weights = torch.empty((T, k), dtype=torch.float32, device=logits.device)
+    _dev(logits, topk_ids, topk_weights)
+    _check(lib().moe_route(_ptr(logits), T, E, k, renormalize, _ptr(topk_ids), _ptr(topk_weights),
+                           _stream(stream, logits.device)))
+    return topk_ids, topk_weights
+
+
+def moe_permute_workspace_bytes(T, E, k) -> int:
+    return lib().moe_permute_workspace_bytes(T, E, k)
+
+
+def moe_permute(topk_ids, x, E, out=None, ws=None, stream=None):
+    """-> dict(counts, offsets, sorted_token_ids, dest_rows, x_perm)."""
+    T, k = topk_ids.shape
+    H = x.shape[1]
+    dev = x.device
+    if out is None:
+        out = dict(counts=torch.empty(E, dtype=torch.int32, device=dev),
+                   offsets=torch.empty(E + 1, dtype=torch.int32, device=dev),
+                   sorted_token_ids=torch.empty(T * k, dtype=torch.int32, device=dev),
+                   dest_rows=torch.empty((T, k), dtype=torch.int32, device=dev),
+                   x_perm=torch.empty((T * k, H), dtype=x.dtype, device=dev))
+    if ws is None:
+        ws = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), dtype=torch.uint8, device=dev)
+    _dev(topk_ids, x, ws, *out.values())
+    _check(lib().moe_permute(_ptr(topk_ids), _ptr(x), T, E, k, H, _dt(x), _ptr(out["counts"]),
+                             _ptr(out["offsets"]), _ptr(out["sorted_token_ids"]), _ptr(out["dest_rows"]),
+                             _ptr(out["x_perm"]), _ptr(ws), ws.numel(), _stream(stream, dev)))
+    return out
+
+
+def moe_grouped_ffn_workspace_bytes(R, E, H, F, dtype) -> int:
+    return lib().moe_grouped_ffn_workspace_bytes(R, E, H, F, DTYPE_F32 if dtype == torch.float32 else DTYPE_BF16)
+
+
+def moe_grouped_ffn(x_perm, offsets, w_gate, w_up, w_down, y_perm=None, ws=None, stream=None):
+    """x_perm [R, H], offsets i32 [E+1] (device), w_gate/w_up [E, F, H], w_down [E, H, F] -> y_perm [R, H]."""
+    R, H = x_perm.shape
+    E, F, _ = w_gate.shape
+    dev = x_perm.device
+    if y_perm is None:
+        y_perm = torch.empty((R, H), dtype=x_perm.dtype, device=dev)
+    if ws is None:
+        ws = torch.empty(max(1, moe_grouped_ffn_workspace_bytes(R, E, H, F, x_perm.dtype)),
+                         dtype=torch.uint8, device=dev)
+    _dev(x_perm, offsets, w_gate, w_up, w_down, y_perm, ws)
+    for w in (w_gate, w_up, w_down):
+        if w.dtype != x_perm.dtype:
+            raise TypeError("weights and activations must share a dtype")
+    _check(lib().moe_grouped_ffn(_ptr(x_perm), _ptr(offsets), R, E, H, F, _ptr(w_gate), _ptr(w_up),
+                                 _ptr(w_down), _dt(x_perm), _ptr(y_perm), _ptr(ws), ws.numel(),
+                                 _stream(stream, dev)))
+    return y_perm
+
+
+def moe_combine(y_perm, dest_rows, topk_weights, y_shared=None, y=None, stream=None):
+    """-> y [T, H] = sum_j w[t, j] y_perm[dest_rows[t, j]] (+ y_shared)."""
+    T, k = dest_rows.shape
+    H = y_perm.shape[1]
+    dev = y_perm.device
+    if y is None:
+        y = torch.empty((T, H), dtype=y_perm.dtype, device=dev)
+    _dev(y_perm, dest_rows, topk_weights, y_shared, y)
+    _check(lib().moe_combine(_ptr(y_perm), _ptr(dest_rows), _ptr(topk_weights), _ptr(y_shared), T, k, H,
+                             _dt(y_perm), _ptr(y), _stream(stream, dev)))
+    return y
+
+
+# --------------------------------------------------------------------------- whole layer
+class MoELayer:
+    """Preallocated buffers for one layer shape; ``run`` issues the calls on one stream
+    with no allocation and no host synchronization."""
+
+    def __init__(self, T, H, E, k, F, Fs=0, dtype=torch.bfloat16, device="cuda"):
+        self.T, self.H, self.E, self.k, self.F, self.Fs = T, H, E, k, F, Fs
+        self.dtype = dtype
+        dev = torch.device(device)
+        R = T * k
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.topk_ids = torch.empty((T, k), **i32)
+        self.topk_weights = torch.empty((T, k), dtype=torch.float32, device=dev)
+        self.perm = dict(counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32),
+                         sorted_token_ids=torch.empty(R, **i32), dest_rows=torch.empty((T, k), **i32),
+                         x_perm=torch.empty((R, H), dtype=dtype, device=dev))
+        self.ws_perm = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), dtype=torch.uint8, device=dev)
+        self.y_perm = torch.empty((R, H), dtype=dtype, device=dev)
+        self.ws_ffn = torch.empty(max(1, moe_grouped_ffn_workspace_bytes(R, E, H, F, dtype)),
+                                  dtype=torch.uint8, device=dev)
+        self.y = torch.empty((T, H), dtype=dtype, device=dev)
+        if Fs:
+            self.shared_offsets = torch.tensor([0, T], **i32)
+            self.y_shared = torch.empty((T, H), dtype=dtype, device=dev)
+            self.ws_shared = torch.empty(max(1, moe_grouped_ffn_workspace_bytes(T, 1, H, Fs, dtype)),
+                                         dtype=torch.uint8, device=dev)
+        else:
+            self.y_shared = None
+
+    def run(self, x, logits, w_gate, w_up, w_down, ws_gate=None, ws_up=None, ws_down=None,
+            renormalize=1, stream=None):
+        moe_route(logits, self.k, renormalize, self.topk_ids, self.topk_weights, stream=stream)
+        moe_permute(self.topk_ids, x, self.E, out=self.perm, ws=self.ws_perm, stream=stream)
+        moe_grouped_ffn(self.perm["x_perm"], self.perm["offsets"], w_gate, w_up, w_down,
+                        y_perm=self.y_perm, ws=self.ws_ffn, stream=stream)
+        if self.Fs:
+            moe_grouped_ffn(x, self.shared_offsets, ws_gate, ws_up, ws_down, y_perm=self.y_shared,
+                            ws=self.ws_shared, stream=stream)
+        moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, self.y_shared, y=self.y,
+                    stream=stream)
+        return self.y

@@ -1,0 +1,135 @@
+// moe_combine: y[t] = sum_j w[t,j] * y_perm[dest_rows[t,j]] (+ y_shared[t]) on gfx950.
+//
+// Gather form: one wavefront per token walks the hidden dimension in 16-byte
+// vectors (8 bf16 or 4 fp32 per lane), loads the token's k expert rows, sums
+// them in fp32 in slot order, adds the shared-expert row last and rounds once.
+// Every output element is written by exactly one lane, so there are no atomics
+// and the result is deterministic.
+#include "common.h"
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWavesPerBlock = kThreads / kWave;
+
+template <bool BF16>
+struct Vec;
+
+template <>
+struct Vec<true> {                 // 8 bf16 in 16 bytes
+  static constexpr int N = 8;
+  __device__ static void unpack(const u32x4& v, float* f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(v[i] << 16);
+      f[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ static u32x4 pack(const float* f) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = pack_bf16x2(f[2 * i], f[2 * i + 1]);
+    return v;
+  }
+};
+
+template <>
+struct Vec<false> {                // 4 fp32 in 16 bytes
+  static constexpr int N = 4;
+  __device__ static void unpack(const u32x4& v, float* f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f[i] = __uint_as_float(v[i]);
+  }
+  __device__ static u32x4 pack(const float* f) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(f[i]);
+    return v;
+  }
+};
+
+template <bool BF16, int UNROLL>
+__global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __restrict__ y_perm,
+                                                          const int32_t* __restrict__ dest,
+                                                          const float* __restrict__ w,
+                                                          const uint8_t* __restrict__ y_shared,
+                                                          int64_t T, int k, int64_t row_bytes,
+                                                          uint8_t* __restrict__ y) {
+  using V = Vec<BF16>;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t t = int64_t(blockIdx.x) * kWavesPerBlock + wv;
+  if (t >= T) return;
+  int32_t rows[kMaxTopK];
+  float wt[kMaxTopK];
+#pragma unroll
+  for (int j = 0; j < kMaxTopK; ++j) {
+    rows[j] = j < k ? dest[t * k + j] : 0;
+    wt[j] = j < k ? w[t * k + j] : 0.f;
+  }
+  const int nvec = int(row_bytes / 16);
+  for (int v0 = lane; v0 < nvec; v0 += kWave * UNROLL) {
+    float acc[UNROLL][V::N];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+      for (int i = 0; i < V::N; ++i) acc[u][i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) {
+      if (j < k) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(y_perm + int64_t(rows[j]) * row_bytes);
+        u32x4 raw[UNROLL];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u)
+          if (v0 + u * kWave < nvec) raw[u] = __builtin_nontemporal_load(src + v0 + u * kWave);
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+          if (v0 + u * kWave < nvec) {
+            float f[V::N];
+            V::unpack(raw[u], f);
+#pragma unroll
+            for (int i = 0; i < V::N; ++i) acc[u][i] = fmaf(wt[j], f[i], acc[u][i]);
+          }
+        }
+      }
+    }
+    if (y_shared != nullptr) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(y_shared + t * row_bytes);
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        if (v0 + u * kWave < nvec) {
+          float f[V::N];
+          V::unpack(__builtin_nontemporal_load(src + v0 + u * kWave), f);
+#pragma unroll
+          for (int i = 0; i < V::N; ++i) acc[u][i] += f[i];
+        }
+      }
+    }
+    u32x4* dst = reinterpret_cast<u32x4*>(y + t * row_bytes);
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+      if (v0 + u * kWave < nvec) dst[v0 + u * kWave] = V::pack(acc[u]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
+                          int64_t T, int k, int H, bool bf16, void* y, hipStream_t s) {
+  const int64_t row_bytes = int64_t(H) * (bf16 ? 2 : 4);
+  const unsigned blocks = unsigned((T + kWavesPerBlock - 1) / kWavesPerBlock);
+  auto yp = static_cast<const uint8_t*>(y_perm);
+  auto ys = static_cast<const uint8_t*>(y_shared);
+  auto yo = static_cast<uint8_t*>(y);
+  if (bf16)
+    hipLaunchKernelGGL((combine_kernel<true, 2>), dim3(blocks), dim3(kThreads), 0, s, yp, dest, w, ys,
+                       T, k, row_bytes, yo);
+  else
+    hipLaunchKernelGGL((combine_kernel<false, 2>), dim3(blocks), dim3(kThreads), 0, s, yp, dest, w, ys,
+                       T, k, row_bytes, yo);
+  return hipGetLastError();
+}
+
+}  // namespace moe

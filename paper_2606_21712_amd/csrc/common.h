@@ -1,0 +1,78 @@
+// Device helpers shared by the gfx950 kernels of the MoE hot path.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+constexpr int kWave = 64;       // CDNA wavefront width
+constexpr int kNumXcd = 8;      // MI355X: 8 accelerator complex dies, workgroups dealt round-robin
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// bf16 <-> fp32 as bit patterns.  Rounding is to nearest even; inputs are finite.
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// Two fp32 -> two bf16 packed in one 32-bit word (low half = a).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return f32_to_bf16_bits(a) | (f32_to_bf16_bits(b) << 16);
+}
+
+// Monotone map of a finite float to uint32 (larger float -> larger integer).
+// -0.0 is first folded onto +0.0 so that the two compare equal, as floats do.
+__device__ __forceinline__ uint32_t orderable(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float from_orderable(uint32_t o) {
+  uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+  return __uint_as_float(u);
+}
+
+// silu(z) = z / (1 + e^-z) in fp32.
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  uint32_t lo = __shfl_xor(uint32_t(v), mask);
+  uint32_t hi = __shfl_xor(uint32_t(v >> 32), mask);
+  return (uint64_t(hi) << 32) | lo;
+}
+
+// Exclusive scan of one int per thread over a 256-thread block; *total = sum.
+// Every thread of the block must call it (it synchronizes the block).
+__device__ __forceinline__ int32_t block_exclusive_scan256(int32_t v, int32_t* total) {
+  __shared__ int32_t wsum[4];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x / kWave;
+  int32_t x = v;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int32_t y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == kWave - 1) wsum[w] = x;
+  __syncthreads();
+  int32_t before = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    before += (i < w) ? wsum[i] : 0;
+    tot += wsum[i];
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x - v;
+}
+
+}  // namespace moe

@@ -1,0 +1,32 @@
+// Internal launchers of the gfx950 kernels behind the C ABI (include/moe.h).
+// Arguments are validated by the caller (moe_abi.cpp) before any launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+constexpr int kMaxTopK = 16;
+constexpr int kMaxExperts = 256;
+
+void route_shape(int E, int* G, int* V);
+hipError_t launch_route(const float* logits, int64_t T, int E, int k, int renorm, int32_t* ids,
+                        float* w, hipStream_t s);
+
+hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, int k, int H, int elt,
+                          int32_t* counts, int32_t* offsets, int32_t* sorted_tok, int32_t* dest,
+                          void* x_perm, int32_t* unit_counts, int64_t units_padded, hipStream_t s);
+
+// Grouped SwiGLU FFN.  mtile_prefix: E + 1 ints of device scratch.
+hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64_t R, int E, int H,
+                           int F, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
+                           uint16_t* y_perm, int32_t* mtile_prefix, uint16_t* h, int num_cu,
+                           hipStream_t s);
+hipError_t launch_ffn_f32(const float* x_perm, const int32_t* offsets, int64_t R, int E, int H, int F,
+                          const float* wg, const float* wu, const float* wd, float* y_perm,
+                          int32_t* mtile_prefix, float* h, hipStream_t s);
+
+hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
+                          int64_t T, int k, int H, bool bf16, void* y, hipStream_t s);
+
+}  // namespace moe

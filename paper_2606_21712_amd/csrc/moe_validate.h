@@ -1,0 +1,38 @@
+// Host-side argument validation for the C ABI in include/moe.h.
+// Plain C++ with no HIP dependency, so it can be built and tested on a machine
+// without a GPU (and under host sanitizers).
+#pragma once
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/moe.h"
+
+namespace moe {
+
+struct Check {
+  moe_status status = MOE_OK;
+  std::string msg;
+  bool ok() const { return status == MOE_OK; }
+};
+
+// Workspace layouts (bytes).  Offsets inside the workspace are 256-byte aligned.
+size_t permute_workspace_bytes(int64_t T, int32_t E, int32_t k);
+size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt);
+size_t ffn_h_offset(int32_t E);            // h [R, F] starts here inside the ffn workspace
+int64_t permute_units(int64_t R);           // count-units (1024 assignments each)
+
+constexpr int64_t kPermuteUnit = 1024;      // assignments per counting unit (one wavefront)
+
+Check validate_route(const float* logits, int64_t T, int32_t E, int32_t k, int32_t renormalize,
+                     const int32_t* ids, const float* w);
+Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, int32_t k, int32_t H,
+                       int dt, const int32_t* counts, const int32_t* offsets, const int32_t* sorted_tok,
+                       const int32_t* dest, const void* x_perm, const void* ws, size_t ws_bytes);
+Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
+                   int32_t F, const void* wg, const void* wu, const void* wd, int dt,
+                   const void* y_perm, const void* ws, size_t ws_bytes);
+Check validate_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
+                       int64_t T, int32_t k, int32_t H, int dt, const void* y);
+
+}  // namespace moe

@@ -1,0 +1,57 @@
+"""Helpers for the GPU parity tests: move generator outputs to the device and
+compare against the oracle.  Nothing here computes any part of the layer."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+
+def log(msg: str):
+    """Name the case before each GPU step (flushed, so it survives a crash)."""
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a: np.ndarray, dev="cuda") -> torch.Tensor:
+    """Host array -> device tensor; uint16 arrays are bf16 bit patterns."""
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(a).to(dev)
+
+
+def to_host(t: torch.Tensor) -> np.ndarray:
+    """Device tensor -> host array; bf16 comes back as uint16 bit patterns."""
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def f64(a: np.ndarray) -> np.ndarray:
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def weight_tol(k: int, E: int) -> float:
+    """Bound on |w_gpu - w_oracle| for gate weights in [0, 1] computed in fp32.
+
+    Each p_j = exp(l_j - l_max) carries at most ~2 ulp (fp32 subtraction rounding
+    amplified by |l_j - l_max| is bounded by the exp's own error for the selected
+    logits), the fp32 sum of n terms adds at most n half-ulps of the sum and the
+    division one more: relative error <= (n + 4) * 2^-24 with n = k (renormalized)
+    or n = 8 + log2(E) (tree sum over all experts).  Weights are <= 1, so this
+    is also an absolute bound."""
+    n = max(k, 8 + int(np.ceil(np.log2(max(E, 2)))))
+    return (n + 4) * 2.0 ** -23
+
+
+def rel_max_err(gpu: np.ndarray, ref: np.ndarray) -> float:
+    """max |gpu - ref| / max |ref| (the layer's parity bound is on this ratio)."""
+    scale = np.abs(ref).max()
+    if scale == 0:
+        return float(np.abs(gpu).max())
+    return float(np.abs(gpu - ref).max() / scale)

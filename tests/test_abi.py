@@ -1,0 +1,120 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every function
+include/moe.h declares, and rejects bad arguments on the host before any launch.
+No call here reaches a kernel: each one fails validation or is a T = 0 no-op."""
+import ctypes
+
+import pytest
+
+import paper_2606_21712_amd as moe
+
+INVALID, UNSUPPORTED, WS_SMALL = 1, 2, 3
+P = 0x10000          # a 16-byte aligned address that is never dereferenced
+S = None             # default stream
+
+
+@pytest.fixture(scope="module")
+def L():
+    return moe.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = moe.exported_symbols()
+    assert {"moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine", "moe_abi_version",
+            "moe_status_string", "moe_last_error", "moe_permute_workspace_bytes",
+            "moe_grouped_ffn_workspace_bytes"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings(L):
+    assert moe.abi_version() == 1
+    for s, name in [(0, b"MOE_OK"), (1, b"MOE_ERR_INVALID_ARGUMENT"), (2, b"MOE_ERR_UNSUPPORTED"),
+                    (3, b"MOE_ERR_WORKSPACE_TOO_SMALL"), (4, b"MOE_ERR_HIP")]:
+        assert L.moe_status_string(s) == name
+    assert L.moe_status_string(99) is not None
+
+
+def route(L, logits=P, T=16, E=8, k=2, renorm=1, ids=P, w=P):
+    return L.moe_route(logits, T, E, k, renorm, ids, w, S)
+
+
+def test_route_validation(L):
+    assert route(L, k=0) == INVALID
+    assert route(L, k=9) == INVALID
+    assert route(L, E=0) == INVALID
+    assert route(L, E=300, k=2) == UNSUPPORTED
+    assert route(L, E=64, k=17) == UNSUPPORTED
+    assert route(L, T=-1) == INVALID
+    assert route(L, T=2**31, k=2) == INVALID                      # T*k > INT32_MAX
+    assert route(L, renorm=2) == INVALID
+    assert route(L, logits=None) == INVALID
+    assert b"logits" in L.moe_last_error()
+    assert route(L, ids=P + 8) == INVALID
+    assert b"aligned" in L.moe_last_error()
+    assert route(L, T=0, logits=None, ids=None, w=None) == 0       # no-op
+
+
+def permute(L, ids=P, x=P, T=16, E=8, k=2, H=64, dt=1, cnt=P, off=P, st=P, dest=P, xp=P, ws=P,
+            ws_bytes=1 << 20):
+    return L.moe_permute(ids, x, T, E, k, H, dt, cnt, off, st, dest, xp, ws, ws_bytes, S)
+
+
+def test_permute_validation(L):
+    assert permute(L, H=96) == INVALID
+    assert permute(L, H=0) == INVALID
+    assert permute(L, dt=7) == UNSUPPORTED
+    assert permute(L, k=3, E=2) == INVALID
+    assert permute(L, x=None) == INVALID
+    assert permute(L, ws_bytes=0) == WS_SMALL
+    assert permute(L, T=0, ids=None, x=None, cnt=None, off=None, st=None, dest=None, xp=None,
+                   ws=None, ws_bytes=0) == 0
+
+
+def test_permute_workspace_size(L):
+    # one int32 count per (unit of 1024 assignments, expert), units padded to 4
+    assert L.moe_permute_workspace_bytes(0, 8, 2) == 0
+    assert L.moe_permute_workspace_bytes(4096, 8, 2) == 8 * 8 * 4
+    assert L.moe_permute_workspace_bytes(131072, 64, 4) == 512 * 64 * 4
+    assert L.moe_permute_workspace_bytes(1, 3, 1) == 256          # 4 units x 3 experts, 256-aligned
+
+
+def ffn(L, xp=P, off=P, R=100, E=8, H=128, F=256, wg=P, wu=P, wd=P, dt=1, yp=P, ws=P, ws_bytes=1 << 30):
+    return L.moe_grouped_ffn(xp, off, R, E, H, F, wg, wu, wd, dt, yp, ws, ws_bytes, S)
+
+
+def test_ffn_validation(L):
+    assert ffn(L, H=100) == INVALID
+    assert ffn(L, F=32) == INVALID
+    assert ffn(L, E=0) == INVALID
+    assert ffn(L, E=257) == UNSUPPORTED
+    assert ffn(L, R=-5) == INVALID
+    assert ffn(L, R=2**31) == INVALID
+    assert ffn(L, dt=3) == UNSUPPORTED
+    assert ffn(L, H=65536, F=32768) == UNSUPPORTED                 # expert matrix > 2 GiB
+    assert ffn(L, wd=None) == INVALID
+    assert b"w_down" in L.moe_last_error()
+    need = L.moe_grouped_ffn_workspace_bytes(100, 8, 128, 256, 1)
+    assert need >= 100 * 256 * 2
+    assert ffn(L, ws_bytes=need - 1) == WS_SMALL
+    assert ffn(L, R=0, xp=None, off=None, wg=None, wu=None, wd=None, yp=None, ws=None, ws_bytes=0) == 0
+    # fp32 h is twice as large
+    assert L.moe_grouped_ffn_workspace_bytes(100, 8, 128, 256, 0) > need
+
+
+def combine(L, yp=P, dest=P, w=P, ys=None, T=16, k=2, H=64, dt=1, y=P):
+    return L.moe_combine(yp, dest, w, ys, T, k, H, dt, y, S)
+
+
+def test_combine_validation(L):
+    assert combine(L, k=0) == INVALID
+    assert combine(L, k=17) == UNSUPPORTED
+    assert combine(L, H=10) == INVALID
+    assert combine(L, y=None) == INVALID
+    assert combine(L, ys=P + 4) == INVALID
+    assert combine(L, T=0, yp=None, dest=None, w=None, y=None) == 0
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        moe.moe_route(torch.zeros(4, 8), 2)

@@ -1,0 +1,184 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Bars (bf16 layers): routing and permutation bit-exact; gate weights within
+weight_tol; y_perm per expert group and y within 2e-2 * max|oracle|.  fp32
+layer: 1e-4 * max|oracle| (fp32 accumulation over K <= 512 rounds at ~1e-6).
+Inputs are the seeded generator's; expected values come only from oracle/."""
+import numpy as np
+import pytest
+import torch
+
+import moegen
+import oracle
+import paper_2606_21712_amd as moe
+from tests.gpu_util import f64, log, rel_max_err, to_dev, to_host, weight_tol
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+F32_TOL = 1e-4
+
+
+def small(name, **kw):
+    return moegen.MoEConfig(name, **kw)
+
+
+# Reduced shapes of the five workloads: several 256-row m-tiles per expert with a
+# ragged tail, ragged feature (F % 128) and hidden (H % 256) tails.
+CASES = {
+    "tiny_f32": moegen.CONFIGS["tiny"],
+    "mixtral_small": small("mixtral_small", T=1500, H=576, E=8, k=2, F=320, seed=11),
+    "zipf_small": small("zipf_small", T=2048, H=256, E=8, k=2, F=256, seed=12, routing="zipf"),
+    "deepseek_small": small("deepseek_small", T=512, H=448, E=64, k=8, F=192, Fs=192, seed=13),
+    "memc_small": small("memc_small", T=4096, H=256, E=64, k=4, F=256, seed=14, routing="lognormal",
+                        pinned_small=(1, 17, 31)),
+    "uniform_router": small("uniform_router", T=300, H=128, E=8, k=3, F=128, seed=15, routing="uniform"),
+    "k1": small("k1", T=700, H=128, E=6, k=1, F=192, seed=16),
+    "k_eq_E": small("k_eq_E", T=260, H=64, E=4, k=4, F=64, seed=17),
+    "T1": small("T1", T=1, H=64, E=8, k=2, F=64, seed=18),
+    "H64_f32": small("H64_f32", T=333, H=64, E=5, k=2, F=64, seed=19, dtype="f32"),
+}
+
+
+_INPUTS = {}
+
+
+def inputs(name):
+    if name not in _INPUTS:
+        _INPUTS[name] = moegen.make_inputs(CASES[name])
+    return _INPUTS[name]
+
+
+def run_layer(I, renormalize=1):
+    c = I.cfg
+    dt = torch.float32 if c.dtype == "f32" else torch.bfloat16
+    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt)
+    shared = (to_dev(I.ws_gate), to_dev(I.ws_up), to_dev(I.ws_down)) if c.Fs else (None, None, None)
+    layer.run(to_dev(I.x), to_dev(I.logits), to_dev(I.w_gate), to_dev(I.w_up), to_dev(I.w_down),
+              *shared, renormalize=renormalize)
+    torch.cuda.synchronize()
+    out = dict(ids=to_host(layer.topk_ids), w=to_host(layer.topk_weights),
+               y_perm=to_host(layer.y_perm), y=to_host(layer.y))
+    out.update({k: to_host(v) for k, v in layer.perm.items()})
+    if c.Fs:
+        out["y_shared"] = to_host(layer.y_shared)
+    return out
+
+
+def oracle_layer(I, renormalize=1):
+    c = I.cfg
+    sh = (I.ws_gate, I.ws_up, I.ws_down) if c.Fs else (None, None, None)
+    return oracle.layer(I.x, I.logits, c.k, I.w_gate, I.w_up, I.w_down, renormalize, *sh)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_layer_parity(name):
+    I = inputs(name)
+    c = I.cfg
+    log(f"[gpu] layer parity {name}: T={c.T} H={c.H} E={c.E} k={c.k} F={c.F} Fs={c.Fs} {c.dtype}")
+    g = run_layer(I)
+    o = oracle_layer(I)
+    # routing and permutation: bit-exact
+    assert np.array_equal(g["ids"], o["ids"])
+    assert np.abs(g["w"] - o["w"]).max() <= weight_tol(c.k, c.E)
+    for key in ("counts", "offsets", "dest_rows", "sorted_token_ids"):
+        assert np.array_equal(g[key], o[key]), key
+    assert np.array_equal(g["x_perm"], o["x_perm"])
+    tol = F32_TOL if c.dtype == "f32" else BF16_TOL
+    # y_perm, per expert group (an error confined to a tiny group must not hide)
+    yp = f64(g["y_perm"])
+    for e in range(c.E):
+        lo, hi = o["offsets"][e], o["offsets"][e + 1]
+        if hi > lo:
+            err = rel_max_err(yp[lo:hi], o["y_perm"][lo:hi])
+            assert err <= tol, (e, hi - lo, err)
+    if c.Fs:
+        assert rel_max_err(f64(g["y_shared"]), o["y_shared"]) <= tol
+    err = rel_max_err(f64(g["y"]), o["y"])
+    log(f"[gpu]   max|dy|/max|y| = {err:.3e}")
+    assert err <= tol
+
+
+@pytest.mark.parametrize("name", ["mixtral_small", "deepseek_small"])
+def test_route_without_renormalize(name):
+    I = inputs(name)
+    c = I.cfg
+    log(f"[gpu] route renormalize=0 {name}")
+    ids, w = moe.moe_route(to_dev(I.logits), c.k, 0)
+    torch.cuda.synchronize()
+    oi, ow = oracle.route(I.logits, c.k, 0)
+    assert np.array_equal(to_host(ids), oi)
+    assert np.abs(to_host(w) - ow).max() <= weight_tol(c.k, c.E)
+
+
+def test_route_ties_and_signed_zero():
+    """Integer-valued logits force ties (lower id wins); -0.0 equals +0.0."""
+    rng = np.random.default_rng(5)
+    for (T, E, k) in [(1000, 8, 2), (513, 64, 8), (77, 256, 16), (64, 3, 3), (200, 100, 7)]:
+        logits = rng.integers(-2, 3, size=(T, E)).astype(np.float32)
+        logits[::7, 0] = -0.0
+        logits[::5, 1] = 0.0
+        log(f"[gpu] route ties T={T} E={E} k={k}")
+        for renorm in (0, 1):
+            ids, w = moe.moe_route(to_dev(logits), k, renorm)
+            torch.cuda.synchronize()
+            oi, ow = oracle.route(logits, k, renorm)
+            assert np.array_equal(to_host(ids), oi)
+            assert np.abs(to_host(w) - ow).max() <= weight_tol(k, E)
+
+
+def test_permute_large_ids_direct():
+    """Permute on ids from brute-force-checkable random expert sets, E = 256."""
+    rng = np.random.default_rng(6)
+    T, E, k, H = 3000, 256, 5, 128
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    x = moegen.round_bf16(rng.standard_normal((T, H)).astype(np.float32))
+    log(f"[gpu] permute E=256 T={T} k={k}")
+    out = moe.moe_permute(to_dev(ids), to_dev(x), E)
+    torch.cuda.synchronize()
+    oc, oo, od, os_, oxp = oracle.permute(ids, x, E)
+    assert np.array_equal(to_host(out["counts"]), oc)
+    assert np.array_equal(to_host(out["offsets"]), oo)
+    assert np.array_equal(to_host(out["dest_rows"]), od)
+    assert np.array_equal(to_host(out["sorted_token_ids"]), os_)
+    assert np.array_equal(to_host(out["x_perm"]), oxp)
+
+
+def test_combine_direct():
+    """Combine alone on random y_perm / weights / shared rows.  Per element,
+    |gpu - oracle| <= 2^-8 * (sum_j |w_j y_j| + |y_s|): one bf16 rounding (2^-9)
+    plus fp32 summation of at most 17 terms."""
+    rng = np.random.default_rng(7)
+    for (T, k, H, shared) in [(999, 4, 192, True), (64, 16, 64, False), (1, 1, 128, True)]:
+        R = T * k
+        yp = moegen.round_bf16(rng.standard_normal((R, H)).astype(np.float32))
+        dest = rng.permutation(R).reshape(T, k).astype(np.int32)
+        w = rng.random((T, k)).astype(np.float32)
+        ys = moegen.round_bf16(rng.standard_normal((T, H)).astype(np.float32)) if shared else None
+        log(f"[gpu] combine T={T} k={k} H={H} shared={shared}")
+        y = moe.moe_combine(to_dev(yp), to_dev(dest), to_dev(w), None if ys is None else to_dev(ys))
+        torch.cuda.synchronize()
+        ref = oracle.combine(yp, dest, w, ys)
+        mag = np.zeros((T, H))
+        for j in range(k):
+            mag += np.abs(w[:, j:j + 1].astype(np.float64) * f64(yp)[dest[:, j]])
+        if ys is not None:
+            mag += np.abs(f64(ys))
+        assert (np.abs(f64(to_host(y)) - ref) <= 2.0 ** -8 * mag + 1e-30).all()
+
+
+def test_zero_tokens_is_a_noop():
+    log("[gpu] T=0")
+    e = torch.empty(0, 8, device="cuda")
+    ids, w = moe.moe_route(e, 2)
+    assert ids.shape == (0, 2)
+    torch.cuda.synchronize()
+
+
+def test_deterministic():
+    I = inputs("memc_small")
+    log("[gpu] determinism memc_small x2")
+    a = run_layer(I)
+    b = run_layer(I)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
