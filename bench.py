@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Throughput of the MoE-layer hot path on one MI355X.
+
+One step = the whole layer (route -> permute -> grouped SwiGLU FFN [-> shared
+expert] -> combine) over one synthetic expert batch whose inputs are already
+resident in HBM.  The default workload is the Mixtral-shaped layer: 4096
+tokens, hidden 4096, 8 experts, top-2, FFN dim 14336, bf16, near-uniform
+routing.  Prints ONE JSON line on stdout; progress goes to stderr.
+
+Per-kernel durations come from the library's own HIP-event profiler, recorded
+on the launch stream inside the timed region.  The roofline figure is for the
+dominant kernel, GEMM-1 (gate/up projections + SwiGLU): algorithmic flops
+4*H*F*R per launch over its average launch duration, against the 2.5 PFLOP/s
+dense bf16 MFMA peak.  The CPU baseline times the fp64 oracle on a bounded
+sample of tokens of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+METRIC = "MoE layer tokens/s + grouped-GEMM TFLOP/s (% bf16 MFMA peak) at 1 MI355X"
+
+# Tokens of each workload the oracle processes for the CPU baseline (10-30 s of host work).
+CPU_SAMPLE = {"tiny": 256, "mixtral4k": 1024, "mixtral32k_zipf": 1024, "deepseek": 1024,
+              "memconstrained": 1024}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def to_dev(a, torch):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to("cuda").view(torch.bfloat16)
+    return torch.from_numpy(a).to("cuda")
+
+
+def cpu_baseline(I, tokens):
+    """Time the fp64 oracle (as it stands) on `tokens` of the workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    c = I.cfg
+    sh = (I.ws_gate, I.ws_up, I.ws_down) if c.Fs else (None, None, None)
+    t0 = time.perf_counter()
+    _, _, y, _ = oracle.token_outputs(tokens, I.x, I.logits, c.k, I.w_gate, I.w_up, I.w_down,
+                                      c.renormalize, *sh)
+    dt = time.perf_counter() - t0
+    return dict(value=len(tokens) / dt, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{len(tokens)} of {c.T} tokens through the whole layer "
+                       f"(fp64 numpy, route + per-expert SwiGLU + combine), {dt:.1f} s"), y
+
+
+def copy_calibration(nbytes: int):
+    """A plain copy of known size: HBM bytes counted by FETCH_SIZE / WRITE_SIZE for it
+    give the scale factor applied to the same counters of the MoE kernels."""
+    import torch
+    src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    dst.copy_(src)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    print(json.dumps({"copy_bytes": nbytes, "ms": ms, "GBps_read_plus_write": 2 * nbytes / ms / 1e6}))
+
+
+def main():
+    import moegen
+
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="mixtral4k", choices=sorted(moegen.CONFIGS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the MoE-layer hot path is built and timed on a "
+              "single MI355X (no collectives or sharding); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_21712_amd as moe
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    moe.lib()                                        # fail loudly if the library is missing
+
+    cfg = moegen.CONFIGS[args.config]
+    c = cfg
+    t0 = time.perf_counter()
+    log(f"generating inputs for {c.name}: T={c.T} H={c.H} E={c.E} k={c.k} F={c.F} Fs={c.Fs} {c.dtype}")
+    I = moegen.make_inputs(cfg)
+    log(f"inputs ready in {time.perf_counter() - t0:.1f} s; copying to the GPU")
+    dt = torch.float32 if c.dtype == "f32" else torch.bfloat16
+    x, logits = to_dev(I.x, torch), to_dev(I.logits, torch)
+    wg, wu, wd = to_dev(I.w_gate, torch), to_dev(I.w_up, torch), to_dev(I.w_down, torch)
+    shared = (to_dev(I.ws_gate, torch), to_dev(I.ws_up, torch), to_dev(I.ws_down, torch)) if c.Fs \
+        else (None, None, None)
+    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        layer.run(x, logits, wg, wu, wd, *shared, renormalize=c.renormalize, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
+
+    moe.profiler_start(args.steps * 16 + 16)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    moe.profiler_stop()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    recs = moe.profiler_records()
+    log(f"timed: {ms:.3f} ms/step")
+
+    # Per-kernel averages.  The routed GEMM launches come first in each step; with a
+    # shared expert the second GEMM-1/GEMM-2 of a step belong to it.
+    per = {}
+    nsteps = args.steps
+    for name, t in recs:
+        per.setdefault(name, []).append(t)
+    kernels = {}
+    for name, ts in per.items():
+        n_per_step = max(1, len(ts) // nsteps)
+        for j in range(n_per_step):
+            sub = ts[j::n_per_step]
+            key = name if j == 0 else f"{name}.shared"
+            kernels[key] = dict(avg_us=1e3 * float(np.mean(sub)), launches=len(sub))
+
+    R = c.R
+    gemm1_flops = 4.0 * c.H * c.F * R
+    g1 = kernels.get("ffn_gemm1_gate_up", {}).get("avg_us")
+    ffn_us = sum(kernels[k]["avg_us"] for k in kernels if k.startswith("ffn_"))
+    peak = PEAK_F32_TFLOPS if c.dtype == "f32" else PEAK_BF16_TFLOPS
+    achieved = gemm1_flops / (g1 * 1e-6) / 1e12 if g1 else None
+    ffn_tflops = c.flops() / (ffn_us * 1e-6) / 1e12 if ffn_us else None
+
+    b = 4 if c.dtype == "f32" else 2
+    bytes_alg = {
+        "route": c.T * c.E * 4 + c.T * c.k * 8,
+        "permute": c.T * c.H * b + R * c.H * b + 3 * R * 4,
+        "combine": R * c.H * b + c.T * c.H * b * (2 if c.Fs else 1) + c.T * c.k * 8,
+    }
+    perm_us = sum(kernels[k]["avg_us"] for k in kernels if k.startswith("permute_"))
+    bw = {}
+    for name, us in (("route", kernels.get("route", {}).get("avg_us")), ("permute", perm_us),
+                     ("combine", kernels.get("combine", {}).get("avg_us"))):
+        if us:
+            gbs = bytes_alg[name] / (us * 1e-6) / 1e9
+            bw[name] = dict(us=round(us, 2), GBps=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 3))
+
+    out = {
+        "metric": METRIC,
+        "value": round(c.T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if c.dtype == "f32" else "bf16",
+        "data": "synthetic (seeded generator; random-init expert weights)",
+        "config": {"workload": c.name, "tokens": c.T, "hidden": c.H, "experts": c.E, "top_k": c.k,
+                   "ffn_dim": c.F, "shared_ffn_dim": c.Fs, "routing": c.routing, "seed": c.seed},
+        "ffn_tflops": round(ffn_tflops, 1) if ffn_tflops else None,
+        "ffn_frac_peak": round(ffn_tflops / peak, 4) if ffn_tflops else None,
+        "roofline": {
+            "kernel": "ffn_gemm1_gate_up",
+            "bound": "mfma",
+            "achieved": round(achieved, 1) if achieved else None,
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4) if achieved else None,
+            "traffic": None,
+            "flops_per_launch": gemm1_flops,
+        },
+        "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
+        "bandwidth": bw,
+    }
+
+    if not args.no_cpu_baseline:
+        n = min(CPU_SAMPLE.get(c.name, 128), c.T)
+        tokens = np.random.default_rng(1234).choice(c.T, size=n, replace=False)
+        log(f"CPU baseline: oracle on {n} tokens")
+        base, y_or = cpu_baseline(I, tokens)
+        out["cpu_baseline"] = base
+        yg = layer.y.float().cpu().numpy()[tokens].astype(np.float64)
+        out["sample_check"] = {"tokens": int(n),
+                               "max_rel_err": float(np.abs(yg - y_or).max() / np.abs(y_or).max())}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -163,6 +163,24 @@ moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float
                        const void* y_shared, int64_t T, int32_t k, int32_t H, moe_dtype dt, void* y,
                        moe_stream stream);
 
+/*
+ * Per-kernel timing (a benchmarking aid, not part of the layer).
+ *
+ * moe_profiler_start(capacity) creates `capacity` pairs of HIP events on the
+ * current device and enables recording: every kernel the library launches
+ * afterwards is bracketed by one pair, recorded on its launch stream, until the
+ * pool is used up or moe_profiler_stop() is called.  Creating the events is the
+ * only allocation, and it happens here, not in the layer calls.  After the
+ * caller synchronizes, moe_profiler_record(i, &name, &ms) returns the i-th
+ * launch's kernel name (a static string) and its duration in milliseconds.
+ * Errors: INVALID_ARGUMENT for capacity < 1 or an index out of range; HIP for
+ * an event failure (e.g. the record's stream has not completed).
+ */
+moe_status moe_profiler_start(int capacity);
+moe_status moe_profiler_stop(void);
+int moe_profiler_count(void);
+moe_status moe_profiler_record(int i, const char** name, float* ms);
+
 #ifdef __cplusplus
 }
 #endif

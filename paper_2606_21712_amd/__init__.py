@@ -19,6 +19,7 @@ __all__ = [
     "MoEError", "lib", "LIB_PATH", "HEADER_PATH", "abi_version", "exported_symbols",
     "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
+    "profiler_start", "profiler_stop", "profiler_records",
     "DTYPE_F32", "DTYPE_BF16",
 ]
 
@@ -56,6 +57,11 @@ _SIGNATURES = {
     "moe_grouped_ffn": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, ctypes.c_int, _P,
                                        _P, _SZ, _P]),
     "moe_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I32, _I32, ctypes.c_int, _P, _P]),
+    "moe_profiler_start": (ctypes.c_int, [ctypes.c_int]),
+    "moe_profiler_stop": (ctypes.c_int, []),
+    "moe_profiler_count": (ctypes.c_int, []),
+    "moe_profiler_record": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
+                                           ctypes.POINTER(ctypes.c_float)]),
 }
 
 
@@ -192,6 +198,27 @@ def moe_combine(y_perm, dest_rows, topk_weights, y_shared=None, y=None, stream=N
     _check(lib().moe_combine(_ptr(y_perm), _ptr(dest_rows), _ptr(topk_weights), _ptr(y_shared), T, k, H,
                              _dt(y_perm), _ptr(y), _stream(stream, dev)))
     return y
+
+
+# --------------------------------------------------------------------------- profiler
+def profiler_start(capacity: int = 4096):
+    """Bracket every following kernel launch of the library with HIP events."""
+    _check(lib().moe_profiler_start(capacity))
+
+
+def profiler_stop():
+    _check(lib().moe_profiler_stop())
+
+
+def profiler_records():
+    """[(kernel name, milliseconds)] of the recorded launches; call after a sync."""
+    out = []
+    name = ctypes.c_char_p()
+    ms = ctypes.c_float()
+    for i in range(lib().moe_profiler_count()):
+        _check(lib().moe_profiler_record(i, ctypes.byref(name), ctypes.byref(ms)))
+        out.append((name.value.decode(), ms.value))
+    return out
 
 
 # --------------------------------------------------------------------------- whole layer

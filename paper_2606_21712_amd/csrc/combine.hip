@@ -124,11 +124,11 @@ hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* 
   auto ys = static_cast<const uint8_t*>(y_shared);
   auto yo = static_cast<uint8_t*>(y);
   if (bf16)
-    hipLaunchKernelGGL((combine_kernel<true, 2>), dim3(blocks), dim3(kThreads), 0, s, yp, dest, w, ys,
-                       T, k, row_bytes, yo);
+    MOE_LAUNCH("combine", (combine_kernel<true, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys,
+               T, k, row_bytes, yo);
   else
-    hipLaunchKernelGGL((combine_kernel<false, 2>), dim3(blocks), dim3(kThreads), 0, s, yp, dest, w, ys,
-                       T, k, row_bytes, yo);
+    MOE_LAUNCH("combine", (combine_kernel<false, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys,
+               T, k, row_bytes, yo);
   return hipGetLastError();
 }
 

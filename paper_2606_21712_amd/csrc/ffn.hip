@@ -348,29 +348,29 @@ hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64
                            int F, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                            uint16_t* y_perm, int32_t* mtile_prefix, uint16_t* h, int num_cu,
                            hipStream_t s) {
-  hipLaunchKernelGGL(tile_prefix_kernel, dim3(1), dim3(256), 0, s, offsets, E, kBM, mtile_prefix);
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
   GemmArgs a1{x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + 127) / 128};
-  hipLaunchKernelGGL(grouped_gemm_bf16_kernel<true>, dim3(grid_for(mtiles_upper * a1.ntiles, num_cu)),
-                     dim3(kGemmThreads), 0, s, a1);
+  MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_bf16_kernel<true>,
+             dim3(grid_for(mtiles_upper * a1.ntiles, num_cu)), dim3(kGemmThreads), s, a1);
   GemmArgs a2{h, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + 255) / 256};
-  hipLaunchKernelGGL(grouped_gemm_bf16_kernel<false>, dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)),
-                     dim3(kGemmThreads), 0, s, a2);
+  MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_bf16_kernel<false>,
+             dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)), dim3(kGemmThreads), s, a2);
   return hipGetLastError();
 }
 
 hipError_t launch_ffn_f32(const float* x_perm, const int32_t* offsets, int64_t R, int E, int H, int F,
                           const float* wg, const float* wu, const float* wd, float* y_perm,
                           int32_t* mtile_prefix, float* h, hipStream_t s) {
-  hipLaunchKernelGGL(tile_prefix_kernel, dim3(1), dim3(256), 0, s, offsets, E, kFM, mtile_prefix);
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, mtile_prefix);
   const int64_t mtiles_upper = (R + int64_t(E) * (kFM - 1)) / kFM;
   GemmArgsF a1{x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + kFN - 1) / kFN};
-  hipLaunchKernelGGL(grouped_gemm_f32_kernel<true>, dim3(unsigned(mtiles_upper * a1.ntiles)), dim3(256),
-                     0, s, a1);
+  MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_f32_kernel<true>, dim3(unsigned(mtiles_upper * a1.ntiles)),
+             dim3(256), s, a1);
   GemmArgsF a2{h, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + kFN - 1) / kFN};
-  hipLaunchKernelGGL(grouped_gemm_f32_kernel<false>, dim3(unsigned(mtiles_upper * a2.ntiles)), dim3(256),
-                     0, s, a2);
+  MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_f32_kernel<false>, dim3(unsigned(mtiles_upper * a2.ntiles)),
+             dim3(256), s, a2);
   return hipGetLastError();
 }
 

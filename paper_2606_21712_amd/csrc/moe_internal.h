@@ -7,6 +7,18 @@
 namespace moe {
 
 constexpr int kMaxTopK = 16;
+
+// Per-kernel event timing (profiler.cpp); no-ops unless moe_profiler_start() ran.
+void prof_begin(hipStream_t s, const char* name);
+void prof_end(hipStream_t s);
+
+// Launch a kernel on `stream`, bracketed by the profiler's events.
+#define MOE_LAUNCH(name, kernel, grid, block, stream, ...)             \
+  do {                                                                 \
+    ::moe::prof_begin(stream, name);                                   \
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, __VA_ARGS__);   \
+    ::moe::prof_end(stream);                                           \
+  } while (0)
 constexpr int kMaxExperts = 256;
 
 void route_shape(int E, int* G, int* V);

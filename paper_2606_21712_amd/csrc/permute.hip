@@ -157,16 +157,15 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
   int nbits = 0;
   while ((1 << nbits) < E) ++nbits;
   const unsigned unit_blocks = unsigned(Upad / kWavesPerBlock);
-  hipLaunchKernelGGL(permute_count_kernel, dim3(unit_blocks), dim3(kThreads), 0, s, ids, R, E, nbits,
-                     Upad, uc);
-  hipLaunchKernelGGL(permute_scan_kernel, dim3(E), dim3(kThreads), 0, s, uc, U, Upad, counts);
-  hipLaunchKernelGGL(permute_rank_kernel, dim3(unit_blocks), dim3(kThreads), 0, s, ids, R, E, k, nbits,
-                     Upad, uc, counts, offsets, dest, sorted_tok);
+  MOE_LAUNCH("permute_count", permute_count_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E,
+             nbits, Upad, uc);
+  MOE_LAUNCH("permute_scan", permute_scan_kernel, dim3(E), dim3(kThreads), s, uc, U, Upad, counts);
+  MOE_LAUNCH("permute_rank", permute_rank_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E, k,
+             nbits, Upad, uc, counts, offsets, dest, sorted_tok);
   const int64_t row_bytes = int64_t(H) * elt;
   const unsigned copy_blocks = unsigned((T + kWavesPerBlock - 1) / kWavesPerBlock);
-  hipLaunchKernelGGL(permute_copy_kernel<4>, dim3(copy_blocks), dim3(kThreads), 0, s,
-                     static_cast<const uint8_t*>(x), T, k, row_bytes, dest,
-                     static_cast<uint8_t*>(x_perm));
+  MOE_LAUNCH("permute_copy", permute_copy_kernel<4>, dim3(copy_blocks), dim3(kThreads), s,
+             static_cast<const uint8_t*>(x), T, k, row_bytes, dest, static_cast<uint8_t*>(x_perm));
   return hipGetLastError();
 }
 

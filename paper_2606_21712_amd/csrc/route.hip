@@ -106,11 +106,11 @@ hipError_t launch_v(const float* logits, int64_t T, int E, int k, int G, int ren
   const int64_t per_block = kRouteThreads / G;
   const int64_t blocks = (T + per_block - 1) / per_block;
   if ((E % 4) == 0 && (V % 4) == 0)
-    hipLaunchKernelGGL((route_kernel<V, (V % 4) == 0>), dim3(unsigned(blocks)), dim3(kRouteThreads),
-                       0, s, logits, T, E, k, G, renorm, ids, w);
+    MOE_LAUNCH("route", (route_kernel<V, (V % 4) == 0>), dim3(unsigned(blocks)), dim3(kRouteThreads),
+               s, logits, T, E, k, G, renorm, ids, w);
   else
-    hipLaunchKernelGGL((route_kernel<V, false>), dim3(unsigned(blocks)), dim3(kRouteThreads), 0, s,
-                       logits, T, E, k, G, renorm, ids, w);
+    MOE_LAUNCH("route", (route_kernel<V, false>), dim3(unsigned(blocks)), dim3(kRouteThreads), s,
+               logits, T, E, k, G, renorm, ids, w);
   return hipGetLastError();
 }
 
