@@ -14,15 +14,18 @@
 // an expert the order is (group of kGroupN n-tiles, m-tile, n-tile): the
 // workgroups of one XCD sweep a few m-tiles against a few n-tiles at a time.
 //
-// bf16 tile: 256 rows x 256 weight rows x 64 k per step, 4 wavefronts (2 x 2),
-// each a 128 x 128 block of v_mfma_f32_32x32x16_bf16 results (16 MFMA tiles).
+// bf16 tile: 256 rows x 256 weight rows x 64 k per step, 8 wavefronts (2 x 4,
+// two per SIMD so one issues MFMAs while the other waits), each a 128 x 64
+// block of v_mfma_f32_32x32x16_bf16 results (8 MFMA tiles).
 // The weight tile is the MFMA A operand and the activation tile the B operand,
 // so each lane ends up holding 4 consecutive output columns of one row: the
 // epilogue stores 8 bytes per lane.  For GEMM-1 the weight tile holds 128
 // gate rows and the 128 up rows of the same features, so silu(g) * u is formed
-// in registers and only h is written.  Tiles are staged through LDS, double
-// buffered, with the 16-byte chunks of each 128-byte row XOR-swizzled by the
-// row index so the MFMA operand reads are free of bank conflicts.
+// in registers and only h is written.  Tiles move from HBM straight into LDS
+// (global_load_lds_dwordx4, no register staging), two stages deep, with the
+// 16-byte chunks of each 128-byte row XOR-swizzled so the MFMA operand reads
+// are free of bank conflicts; operand fragments are double-buffered in
+// registers so LDS latency hides behind the previous sub-step's MFMAs.
 #include "common.h"
 #include "moe_internal.h"
 
@@ -62,7 +65,7 @@ constexpr int kBK = 64;                   // k per pipeline step
 constexpr int kRowBytes = kBK * 2;        // one tile row in LDS: 128 bytes = 8 chunks of 16
 constexpr int kOpBytes = 256 * kRowBytes; // one operand tile: 32 KB
 constexpr int kStageBytes = 2 * kOpBytes;
-constexpr int kGemmThreads = 256;
+constexpr int kGemmThreads = 512;        // 8 wavefronts: 2 (m) x 4 (n), two per SIMD
 constexpr int kGroupN = 8;
 
 struct GemmArgs {
@@ -75,23 +78,46 @@ struct GemmArgs {
   int E, K, N, ntiles;
 };
 
+// First tile row of a wavefront's n-subtile ni (0..1).  GEMM-1: ni = 0 is 32
+// gate features, ni = 1 the up rows of the same features.
 template <bool SWIGLU>
 __device__ __forceinline__ int wave_nrow(int wn, int ni) {
-  if (SWIGLU) return (ni >= 2 ? 128 : 0) + wn * 64 + (ni & 1) * 32;
-  return wn * 128 + ni * 32;
+  if (SWIGLU) return ni * 128 + wn * 32;
+  return wn * 64 + ni * 32;
 }
+
+// LDS layout of one operand tile: 256 rows x 128 bytes (64 bf16 of k), the
+// sixteen-byte chunk c of row r stored at chunk position c ^ ((r >> 1) & 7).
+// gfx950 serves a 16-byte-per-lane LDS read 16 lanes at a time from 64 banks;
+// the 16 rows such a group touches then land on 16 distinct 16-byte slots.
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+// gfx9 s_waitcnt immediate with only vmcnt(0): expcnt and lgkmcnt left at their maxima.
+constexpr int kWaitVm0 = 0x0F70;
+// Buffer resource word 3 for raw (unformatted, stride 0) buffer loads on gfx9.
+constexpr int kBufFlags = 0x00020000;
 
 template <bool SWIGLU>
 __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * kStageBytes];
+  // Two pipeline stages, each [weight tile | activation tile].  They are filled by
+  // direct global->LDS loads; two distinct objects let the compiler tell them apart.
+  __shared__ __attribute__((aligned(1024))) uint8_t st0[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1[kStageBytes];
   __shared__ int32_t s_pref[kMaxExperts + 1];
   __shared__ int32_t s_off[kMaxExperts + 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int wm = wave >> 2, wn = wave & 3;
 
+  // The stages are written only by the LDS-DMA loads, which the compiler does not
+  // count as stores to them; this never-taken store keeps their reads from being
+  // folded away as reads of uninitialized memory.
+  if (p.E < 0) {
+    st0[tid] = 0;
+    st1[tid] = 0;
+  }
   for (int i = tid; i <= p.E; i += kGemmThreads) {
     s_pref[i] = p.mtile_prefix[i];
     s_off[i] = p.offsets[i];
@@ -101,6 +127,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const int NT = p.ntiles;
   const int K = p.K;
   const int N = p.N;
+  const int KT = K / kBK;
   const int64_t total = int64_t(s_pref[p.E]) * NT;
   const int xcd = blockIdx.x % kNumXcd;
   const int slot = blockIdx.x / kNumXcd;
@@ -109,134 +136,159 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const int64_t chunk_lo = int64_t(xcd) * per;
   const int64_t chunk_hi = chunk_lo + per < total ? chunk_lo + per : total;
 
-  // Global -> LDS staging: pass i moves rows i*32 + (tid / 8), 16-byte chunk tid % 8.
-  const int lr = tid >> 3;
-  const int lc = tid & 7;
-  const uint32_t lds_store = uint32_t(lr * kRowBytes + ((lc ^ (lr & 7)) << 4));
-  // MFMA operand reads: row (lane % 32) of a 32-row block, chunk 2*s + lane / 32.
-  const uint32_t lds_read_row = uint32_t((lane & 31) * kRowBytes);
-  const int sw = lane & 7;
+  // DMA: wave w's pass i fills the 1 KB block blk = 8*i + w (tile rows 8*blk..8*blk+7);
+  // lane q lands at byte 16*q of the block: row 8*blk + q/8, chunk position q%8.
+  const int qrow = lane >> 3;
+  const int qpos = lane & 7;
+  // MFMA operand reads: row (lane % 32) of a 32-row block, k-chunk 2*s + lane / 32.
+  const int rrow = lane & 31;
   const int khalf = lane >> 5;
 
   for (int64_t L = chunk_lo + slot; L < chunk_hi; L += slots) {
-    // ---- decode the tile
-    const int e = find_expert(s_pref, p.E, L / NT);
-    const int mt_e = s_pref[e + 1] - s_pref[e];
-    const int64_t local = L - int64_t(s_pref[e]) * NT;
+    // ---- decode the tile (wave-uniform values, moved to scalar registers)
+    const int e = __builtin_amdgcn_readfirstlane(find_expert(s_pref, p.E, L / NT));
+    const int pe = __builtin_amdgcn_readfirstlane(s_pref[e]);
+    const int mt_e = __builtin_amdgcn_readfirstlane(s_pref[e + 1]) - pe;
+    const int64_t local = L - int64_t(pe) * NT;
     const int64_t gsize = int64_t(mt_e) * kGroupN;
     const int ng = int(local / gsize);
     const int rem = int(local - int64_t(ng) * gsize);
     const int gw = min(kGroupN, NT - ng * kGroupN);
     const int mt = rem / gw;
     const int nt = ng * kGroupN + rem % gw;
-    const int row0 = s_off[e] + mt * kBM;
-    const int row_end = s_off[e + 1];
+    const int row0 = __builtin_amdgcn_readfirstlane(s_off[e]) + mt * kBM;
+    const int row_end = __builtin_amdgcn_readfirstlane(s_off[e + 1]);
 
-    // ---- per-thread global sources (byte offsets, rows clamped into range)
-    const uint8_t* abase = reinterpret_cast<const uint8_t*>(p.act) + int64_t(row0) * K * 2;
-    const int64_t wexp = int64_t(e) * N * K * 2;
-    const uint8_t* wbase0 = reinterpret_cast<const uint8_t*>(p.w0) + wexp;
-    const uint8_t* wbase1 = reinterpret_cast<const uint8_t*>(SWIGLU ? p.w1 : p.w0) + wexp;
+    // ---- buffer resources: rows past the group end (activations) or past N
+    // (weights) fall outside num_records and load as zeros.
+    const int arows = min(kBM, row_end - row0);
     const int n0 = SWIGLU ? nt * 128 : nt * 256;
-    uint32_t aoff[8], woff[8];
+    const int wrows = SWIGLU ? min(128, N - n0) : min(256, N - n0);
+    const int64_t rowb = int64_t(K) * 2;
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(p.act) + int64_t(row0) * K, 0, int(arows * rowb), kBufFlags);
+    const int64_t wfirst = (int64_t(e) * N + n0) * K;
+    const __amdgpu_buffer_rsrc_t rw0 = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
+    const __amdgpu_buffer_rsrc_t rw1 = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(SWIGLU ? p.w1 : p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
+    // Per-lane byte offsets of the 4 DMA passes per operand (constant over the k loop).
+    uint32_t aoff[4], woff[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = i * 32 + lr;
-      const int ar = min(row0 + r, row_end - 1) - row0;
-      aoff[i] = uint32_t(ar) * uint32_t(K * 2) + uint32_t(lc * 16);
-      const int wr = SWIGLU ? min(n0 + (i & 3) * 32 + lr, N - 1) : min(n0 + r, N - 1);
-      woff[i] = uint32_t(wr) * uint32_t(K * 2) + uint32_t(lc * 16);
+    for (int i = 0; i < 4; ++i) {
+      const int r = (8 * i + wave) * 8 + qrow;                  // tile row this lane fills
+      const uint32_t cb = uint32_t(swz(r, qpos) * 16);          // its logical chunk, in bytes
+      aoff[i] = uint32_t(r) * uint32_t(rowb) + cb;
+      // GEMM-1: tile rows 0..127 are gate features n0.., rows 128..255 the same up features.
+      woff[i] = uint32_t(SWIGLU ? (r & 127) : r) * uint32_t(rowb) + cb;
     }
 
-    f32x16 acc[4][4];
+    auto issue = [&](uint8_t* stage, int kt) {
+      const int kb = kt * kRowBytes;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int blk = 8 * i + wave;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds((SWIGLU && i >= 2) ? rw1 : rw0, stage + blk * 1024, 16,
+                                                 woff[i], kb, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
+      }
+    };
+
+    f32x16 acc[4][2];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
+      for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[mi][ni][q] = 0.f;
 
-    u32x4 ga[8], gw8[8];
-    auto gload = [&](int kt) {
-      const uint32_t kb = uint32_t(kt) * kRowBytes;
+    auto frags = [&](const uint8_t* stage, int s, bf16x8* wf, bf16x8* xf) {
+      const int c = 2 * s + khalf;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        ga[i] = *reinterpret_cast<const u32x4*>(abase + aoff[i] + kb);
-        const uint8_t* wb = (SWIGLU && i >= 4) ? wbase1 : wbase0;
-        gw8[i] = *reinterpret_cast<const u32x4*>(wb + woff[i] + kb);
+      for (int ni = 0; ni < 2; ++ni) {
+        const int row = wave_nrow<SWIGLU>(wn, ni) + rrow;
+        wf[ni] = *reinterpret_cast<const bf16x8*>(stage + row * kRowBytes + swz(row, c) * 16);
+      }
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) {
+        const int row = wm * 128 + mi * 32 + rrow;
+        xf[mi] = *reinterpret_cast<const bf16x8*>(stage + kOpBytes + row * kRowBytes + swz(row, c) * 16);
       }
     };
-    auto lstore = [&](int buf) {
-      uint8_t* sW = smem + buf * kStageBytes;
-      uint8_t* sX = sW + kOpBytes;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        *reinterpret_cast<u32x4*>(sW + i * 32 * kRowBytes + lds_store) = gw8[i];
-        *reinterpret_cast<u32x4*>(sX + i * 32 * kRowBytes + lds_store) = ga[i];
-      }
-    };
-
-    const int KT = K / kBK;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < KT) gload(kt + 1);
-      const uint8_t* sW = smem + buf * kStageBytes;
-      const uint8_t* sX = sW + kOpBytes;
+    auto compute = [&](const uint8_t* stage) {
+      bf16x8 wf[2][2], xf[2][4];
+      frags(stage, 0, wf[0], xf[0]);
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        const uint32_t coff = uint32_t(((2 * s + khalf) ^ sw) << 4);
-        bf16x8 wf[4], xf[4];
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          wf[ni] = *reinterpret_cast<const bf16x8*>(sW + wave_nrow<SWIGLU>(wn, ni) * kRowBytes +
-                                                    lds_read_row + coff);
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-          xf[mi] = *reinterpret_cast<const bf16x8*>(sX + (wm * 128 + mi * 32) * kRowBytes +
-                                                    lds_read_row + coff);
+        if (s < 3) frags(stage, s + 1, wf[(s + 1) & 1], xf[(s + 1) & 1]);
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-          for (int ni = 0; ni < 4; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ni], xf[mi], acc[mi][ni], 0, 0, 0);
+          for (int ni = 0; ni < 2; ++ni)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s & 1][ni], xf[s & 1][mi],
+                                                                  acc[mi][ni], 0, 0, 0);
+        // Issue order: the next sub-step's 6 LDS reads spread between this one's MFMAs.
+        if (s < 3) {
+#pragma unroll
+          for (int i = 0; i < 6; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        } else {
+          __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        }
       }
-      if (kt + 1 < KT) lstore(buf ^ 1);
+    };
+    // One k-step: wait for this stage's loads (own lanes, then all waves via the
+    // barrier, which also frees the other stage), start the next step's loads into
+    // the other stage, then run the MFMAs of this one.
+    auto step = [&](uint8_t* cur, uint8_t* nxt, int kt) {
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 1 < KT) issue(nxt, kt + 1);
+      compute(cur);
+    };
+
+    issue(st0, 0);
+    int kt = 0;
+    for (; kt + 2 <= KT; kt += 2) {
+      step(st0, st1, kt);
+      step(st1, st0, kt + 1);
     }
+    if (kt < KT) step(st0, st1, kt);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();              // every wave is done with both stages before the next tile
 
     // ---- epilogue: lane holds columns n + 8*blk + 4*khalf + {0..3} of row (lane % 32)
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) {
-      const int row = row0 + wm * 128 + mi * 32 + (lane & 31);
+      const int row = row0 + wm * 128 + mi * 32 + rrow;
       if (row < row_end) {
         uint16_t* orow = p.out + int64_t(row) * N;
         if (SWIGLU) {
 #pragma unroll
-          for (int ni = 0; ni < 2; ++ni) {
+          for (int blk = 0; blk < 4; ++blk) {
+            const int f = n0 + wn * 32 + blk * 8 + khalf * 4;
+            if (f < N) {
+              float hv[4];
 #pragma unroll
-            for (int blk = 0; blk < 4; ++blk) {
-              const int f = n0 + wn * 64 + ni * 32 + blk * 8 + khalf * 4;
-              if (f < N) {
-                float hv[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                  hv[q] = silu(acc[mi][ni][blk * 4 + q]) * acc[mi][ni + 2][blk * 4 + q];
-                u32x2 pk;
-                pk[0] = pack_bf16x2(hv[0], hv[1]);
-                pk[1] = pack_bf16x2(hv[2], hv[3]);
-                *reinterpret_cast<u32x2*>(orow + f) = pk;
-              }
+              for (int q = 0; q < 4; ++q)
+                hv[q] = silu(acc[mi][0][blk * 4 + q]) * acc[mi][1][blk * 4 + q];
+              u32x2 pk;
+              pk[0] = pack_bf16x2(hv[0], hv[1]);
+              pk[1] = pack_bf16x2(hv[2], hv[3]);
+              *reinterpret_cast<u32x2*>(orow + f) = pk;
             }
           }
         } else {
 #pragma unroll
-          for (int ni = 0; ni < 4; ++ni) {
+          for (int ni = 0; ni < 2; ++ni) {
 #pragma unroll
             for (int blk = 0; blk < 4; ++blk) {
-              const int n = n0 + wn * 128 + ni * 32 + blk * 8 + khalf * 4;
+              const int n = n0 + wn * 64 + ni * 32 + blk * 8 + khalf * 4;
               if (n < N) {
                 u32x2 pk;
                 pk[0] = pack_bf16x2(acc[mi][ni][blk * 4 + 0], acc[mi][ni][blk * 4 + 1]);
