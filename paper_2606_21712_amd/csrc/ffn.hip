@@ -5,14 +5,17 @@
 // for every row r of expert e's group.  Both operands are K-contiguous.
 //
 // Tile scheduling.  A tiny kernel turns the device-side offsets into a prefix
-// of m-tiles per expert (no host readback).  The GEMM kernels are persistent:
-// each workgroup walks a strided range of the flattened tile list, in which an
-// expert's tiles are contiguous, so a hot expert simply owns more tiles and an
-// empty one owns none.  Workgroups are dealt to the 8 XCDs round-robin; the
-// list is cut into 8 contiguous chunks, one per XCD, so tiles that share
-// weight and activation panels run on the same XCD and share its L2.  Inside
-// an expert the order is (group of kGroupN n-tiles, m-tile, n-tile): the
-// workgroups of one XCD sweep a few m-tiles against a few n-tiles at a time.
+// of m-tiles per expert (no host readback) and zeroes the tile queues.  The
+// GEMM kernels are persistent, one workgroup per compute unit: each claims
+// tiles from an atomic queue over the flattened tile list, in which an
+// expert's tiles are contiguous, so a hot expert simply owns more tiles, an
+// empty one owns none, and cheap and costly tiles balance dynamically.  Inside
+// an expert the order is (group of kGroupN n-tiles, m-tile, n-tile), so the
+// tiles in flight at any moment share a few weight and activation panels in
+// L2 and in the Infinity Cache.  (Cutting the list into one chunk per XCD, or
+// dealing XCDs residue classes of it, measured 2-5% slower on these shapes:
+// the last-level cache shared by all XCDs serves the panels better when the
+// whole GPU works on one compact front of the tile list.)
 //
 // bf16 tile: 256 rows x 256 weight rows x 64 k per step, 8 wavefronts (2 x 4,
 // two per SIMD so one issues MFMAs while the other waits), each a 128 x 64
@@ -33,10 +36,14 @@ namespace moe {
 namespace {
 
 // ----------------------------------------------------------------------------- tile prefix
+constexpr int kQueueInts = 2;             // tile counters: GEMM-1's, then GEMM-2's
+
 // prefix[e] = sum_{e' < e} ceil(count[e'] / bm), prefix[E] = total.  One block of 256.
 __global__ __launch_bounds__(256) void tile_prefix_kernel(const int32_t* __restrict__ offsets, int E,
-                                                         int bm, int32_t* __restrict__ prefix) {
+                                                         int bm, int32_t* __restrict__ prefix,
+                                                         int32_t* __restrict__ queues) {
   const int e = threadIdx.x;
+  if (queues != nullptr && e < kQueueInts) queues[e] = 0;      // tile queues of both GEMMs
   int32_t mt = 0;
   if (e < E) {
     const int32_t c = offsets[e + 1] - offsets[e];
@@ -69,6 +76,7 @@ constexpr int kGemmThreads = 512;        // 8 wavefronts: 2 (m) x 4 (n), two per
 constexpr int kGroupN = 8;
 
 struct GemmArgs {
+  int32_t* queue;                 // tile counter, zeroed by tile_prefix_kernel
   const uint16_t* act;            // [R, K]
   const uint16_t* w0;             // [E, N, K] (GEMM-1: W_gate; GEMM-2: W_down)
   const uint16_t* w1;             // [E, N, K] (GEMM-1: W_up)
@@ -105,6 +113,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   __shared__ __attribute__((aligned(1024))) uint8_t st1[kStageBytes];
   __shared__ int32_t s_pref[kMaxExperts + 1];
   __shared__ int32_t s_off[kMaxExperts + 1];
+  __shared__ int32_t s_claim[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -129,12 +138,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const int N = p.N;
   const int KT = K / kBK;
   const int64_t total = int64_t(s_pref[p.E]) * NT;
-  const int xcd = blockIdx.x % kNumXcd;
-  const int slot = blockIdx.x / kNumXcd;
-  const int slots = gridDim.x / kNumXcd;
-  const int64_t per = (total + kNumXcd - 1) / kNumXcd;
-  const int64_t chunk_lo = int64_t(xcd) * per;
-  const int64_t chunk_hi = chunk_lo + per < total ? chunk_lo + per : total;
+  // Tiles are handed out by one queue in the global tile order: a workgroup
+  // claims the next tile with one atomic, so faster workgroups take more tiles
+  // and a tile's cost (full or tail m-tile, long or short K) never unbalances the
+  // grid.  The claim for the following tile is made while the current one runs.
+  if (tid == 0) s_claim[0] = atomicAdd(p.queue, 1);
+  __syncthreads();
 
   // DMA: wave w's pass i fills the 1 KB block blk = 8*i + w (tile rows 8*blk..8*blk+7);
   // lane q lands at byte 16*q of the block: row 8*blk + q/8, chunk position q%8.
@@ -144,7 +153,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const int rrow = lane & 31;
   const int khalf = lane >> 5;
 
-  for (int64_t L = chunk_lo + slot; L < chunk_hi; L += slots) {
+  for (int it = 0;; ++it) {
+    const int64_t L = s_claim[it & 1];
+    if (L >= total) break;                                      // uniform: every wave leaves
+    if (tid == 0) s_claim[(it + 1) & 1] = atomicAdd(p.queue, 1);
     // ---- decode the tile (wave-uniform values, moved to scalar registers)
     const int e = __builtin_amdgcn_readfirstlane(find_expert(s_pref, p.E, L / NT));
     const int pe = __builtin_amdgcn_readfirstlane(s_pref[e]);
@@ -243,13 +255,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     // One k-step: wait for this stage's loads (own lanes, then all waves via the
     // barrier, which also frees the other stage), start the next step's loads into
     // the other stage, then run the MFMAs of this one.
+    // A wavefront whose 128 rows all lie past the group end (the tail m-tile of
+    // a group) still loads and synchronizes but skips its MFMAs: the other wave
+    // on its SIMD then has the matrix core to itself.
+    const bool active = row0 + wm * 128 < row_end;
     auto step = [&](uint8_t* cur, uint8_t* nxt, int kt) {
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
       if (kt + 1 < KT) issue(nxt, kt + 1);
-      compute(cur);
+      if (active) compute(cur);
     };
 
     issue(st0, 0);
@@ -387,26 +403,26 @@ __global__ __launch_bounds__(256) void grouped_gemm_f32_kernel(GemmArgsF p) {
   }
 }
 
+// One persistent workgroup per compute unit (fewer for small problems).
 int grid_for(int64_t upper_tiles, int num_cu) {
-  int64_t g = upper_tiles < num_cu ? upper_tiles : num_cu;
-  g = (g + kNumXcd - 1) / kNumXcd * kNumXcd;     // whole XCD rounds
-  if (g < kNumXcd) g = kNumXcd;
-  return int(g);
+  const int64_t g = upper_tiles < num_cu ? upper_tiles : num_cu;
+  return int(g < 1 ? 1 : g);
 }
 
 }  // namespace
 
 hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64_t R, int E, int H,
                            int F, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
-                           uint16_t* y_perm, int32_t* mtile_prefix, uint16_t* h, int num_cu,
-                           hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix);
+                           uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint16_t* h,
+                           int num_cu, hipStream_t s) {
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix,
+             queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
-  GemmArgs a1{x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + 127) / 128};
+  GemmArgs a1{queues, x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + 127) / 128};
   MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_bf16_kernel<true>,
              dim3(grid_for(mtiles_upper * a1.ntiles, num_cu)), dim3(kGemmThreads), s, a1);
-  GemmArgs a2{h, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + 255) / 256};
+  GemmArgs a2{queues + 1, h, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + 255) / 256};
   MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_bf16_kernel<false>,
              dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)), dim3(kGemmThreads), s, a2);
   return hipGetLastError();
@@ -415,7 +431,8 @@ hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64
 hipError_t launch_ffn_f32(const float* x_perm, const int32_t* offsets, int64_t R, int E, int H, int F,
                           const float* wg, const float* wu, const float* wd, float* y_perm,
                           int32_t* mtile_prefix, float* h, hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, mtile_prefix);
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, mtile_prefix,
+             static_cast<int32_t*>(nullptr));
   const int64_t mtiles_upper = (R + int64_t(E) * (kFM - 1)) / kFM;
   GemmArgsF a1{x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + kFN - 1) / kFN};
   MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_f32_kernel<true>, dim3(unsigned(mtiles_upper * a1.ntiles)),

@@ -107,6 +107,7 @@ moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, in
                                    y_perm, ws, ws_bytes);
   if (!c.ok() || R == 0) return finish(c);
   auto* prefix = static_cast<int32_t*>(ws);
+  auto* queues = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(ws) + moe::ffn_queue_offset(E));
   void* h = static_cast<uint8_t*>(ws) + moe::ffn_h_offset(E);
   if (dt == MOE_DTYPE_F32) {
     return hip_status(
@@ -124,7 +125,7 @@ moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, in
       moe::launch_ffn_bf16(static_cast<const uint16_t*>(x_perm), expert_offsets, R, E, H, F,
                            static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
                            static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm),
-                           prefix, static_cast<uint16_t*>(h), ncu, stream_of(stream)));
+                           prefix, queues, static_cast<uint16_t*>(h), ncu, stream_of(stream)));
 }
 
 moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float* topk_weights,

@@ -87,7 +87,8 @@ size_t permute_workspace_bytes(int64_t T, int32_t E, int32_t k) {
   return align256(size_t(units) * size_t(E) * sizeof(int32_t));
 }
 
-size_t ffn_h_offset(int32_t E) { return align256(size_t(E + 1) * sizeof(int32_t)); }
+size_t ffn_queue_offset(int32_t E) { return align256(size_t(E + 1) * sizeof(int32_t)); }
+size_t ffn_h_offset(int32_t E) { return ffn_queue_offset(E) + 256; }
 
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt) {
   (void)H;
