@@ -34,8 +34,26 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 METRIC = "MoE layer tokens/s + grouped-GEMM TFLOP/s (% bf16 MFMA peak) at 1 MI355X"
 
 # Tokens of each workload the oracle processes for the CPU baseline (10-30 s of host work).
-CPU_SAMPLE = {"tiny": 256, "mixtral4k": 1024, "mixtral32k_zipf": 1024, "deepseek": 1024,
-              "memconstrained": 1024}
+CPU_SAMPLE = {"tiny": 256, "mixtral4k": 4096, "mixtral32k_zipf": 4096, "deepseek": 2048,
+              "memconstrained": 4096}
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per GEMM-1 launch from the committed counter summary, or None when
+    the summary is for another workload or the grouped-GEMM source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"ffn_gemm1_gate_up_{workload}_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2606_21712_amd", "csrc", "ffn.hip")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.split(":")[0] in ("source_sha256", "gemm1_traffic_bytes_per_launch"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    return float(fields["gemm1_traffic_bytes_per_launch"])
 
 
 def log(msg):
@@ -211,7 +229,7 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4) if achieved else None,
-            "traffic": None,
+            "traffic": measured_traffic(c.name),
             "flops_per_launch": gemm1_flops,
         },
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
