@@ -29,6 +29,8 @@
 // 16-byte chunks of each 128-byte row XOR-swizzled so the MFMA operand reads
 // are free of bank conflicts; operand fragments are double-buffered in
 // registers so LDS latency hides behind the previous sub-step's MFMAs.
+#include <algorithm>
+
 #include "common.h"
 #include "moe_internal.h"
 
@@ -74,6 +76,7 @@ constexpr int kOpBytes = 256 * kRowBytes; // one operand tile: 32 KB
 constexpr int kStageBytes = 2 * kOpBytes;
 constexpr int kGemmThreads = 512;        // 8 wavefronts: 2 (m) x 4 (n), two per SIMD
 constexpr int kGroupN = 8;
+constexpr int kGroupM = 4;
 
 struct GemmArgs {
   int32_t* queue;                 // tile counter, zeroed by tile_prefix_kernel
@@ -81,9 +84,10 @@ struct GemmArgs {
   const uint16_t* w0;             // [E, N, K] (GEMM-1: W_gate; GEMM-2: W_down)
   const uint16_t* w1;             // [E, N, K] (GEMM-1: W_up)
   uint16_t* out;                  // [R, N]
+  float* partial;                 // [ksplit, R, N] fp32 when ksplit > 1 (GEMM-2 only)
   const int32_t* offsets;         // [E + 1]
   const int32_t* mtile_prefix;    // [E + 1]
-  int E, K, N, ntiles;
+  int E, K, N, ntiles, R, ksplit;
 };
 
 // First tile row of a wavefront's n-subtile ni (0..1).  GEMM-1: ni = 0 is 32
@@ -137,7 +141,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const int K = p.K;
   const int N = p.N;
   const int KT = K / kBK;
-  const int64_t total = int64_t(s_pref[p.E]) * NT;
+  const int ksplit = p.ksplit;
+  const int64_t total = int64_t(s_pref[p.E]) * NT * ksplit;
   // Tiles are handed out by one queue in the global tile order: a workgroup
   // claims the next tile with one atomic, so faster workgroups take more tiles
   // and a tile's cost (full or tail m-tile, long or short K) never unbalances the
@@ -157,17 +162,27 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     const int64_t L = s_claim[it & 1];
     if (L >= total) break;                                      // uniform: every wave leaves
     if (tid == 0) s_claim[(it + 1) & 1] = atomicAdd(p.queue, 1);
-    // ---- decode the tile (wave-uniform values, moved to scalar registers)
-    const int e = __builtin_amdgcn_readfirstlane(find_expert(s_pref, p.E, L / NT));
+    // ---- decode the tile (wave-uniform values, moved to scalar registers).
+    // With a k split, the ksplit pieces of one output tile are adjacent entries.
+    const int64_t Lt = L / ksplit;
+    const int split = int(L - Lt * ksplit);
+    const int kt0 = split * KT / ksplit;
+    const int kt1 = (split + 1) * KT / ksplit;
+    const int e = __builtin_amdgcn_readfirstlane(find_expert(s_pref, p.E, Lt / NT));
     const int pe = __builtin_amdgcn_readfirstlane(s_pref[e]);
     const int mt_e = __builtin_amdgcn_readfirstlane(s_pref[e + 1]) - pe;
-    const int64_t local = L - int64_t(pe) * NT;
-    const int64_t gsize = int64_t(mt_e) * kGroupN;
-    const int ng = int(local / gsize);
-    const int rem = int(local - int64_t(ng) * gsize);
-    const int gw = min(kGroupN, NT - ng * kGroupN);
-    const int mt = rem / gw;
-    const int nt = ng * kGroupN + rem % gw;
+    const int64_t local = Lt - int64_t(pe) * NT;
+    // Inside an expert: blocks of up to kGroupM m-tiles, each swept in groups of
+    // kGroupN n-tiles with the m-tile varying fastest, so the tiles in flight
+    // share a few weight and activation panels.
+    const int64_t bsz = int64_t(kGroupM) * NT;
+    const int mbi = int(local / bsz);
+    const int rem = int(local - int64_t(mbi) * bsz);
+    const int bm = min(kGroupM, mt_e - mbi * kGroupM);
+    const int ng = rem / (bm * kGroupN);
+    const int rem2 = rem - ng * bm * kGroupN;
+    const int mt = mbi * kGroupM + rem2 % bm;
+    const int nt = ng * kGroupN + rem2 / bm;
     const int row0 = __builtin_amdgcn_readfirstlane(s_off[e]) + mt * kBM;
     const int row_end = __builtin_amdgcn_readfirstlane(s_off[e + 1]);
 
@@ -264,17 +279,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
-      if (kt + 1 < KT) issue(nxt, kt + 1);
+      if (kt + 1 < kt1) issue(nxt, kt + 1);
       if (active) compute(cur);
     };
 
-    issue(st0, 0);
-    int kt = 0;
-    for (; kt + 2 <= KT; kt += 2) {
+    issue(st0, kt0);
+    int kt = kt0;
+    for (; kt + 2 <= kt1; kt += 2) {
       step(st0, st1, kt);
       step(st1, st0, kt + 1);
     }
-    if (kt < KT) step(st0, st1, kt);
+    if (kt < kt1) step(st0, st1, kt);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();              // every wave is done with both stages before the next tile
 
@@ -299,6 +314,22 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
               *reinterpret_cast<u32x2*>(orow + f) = pk;
             }
           }
+        } else if (ksplit > 1) {
+          // One piece of a k split: fp32 partial sums, reduced in piece order later.
+          float* prow = p.partial + (int64_t(split) * p.R + row) * N;
+#pragma unroll
+          for (int ni = 0; ni < 2; ++ni) {
+#pragma unroll
+            for (int blk = 0; blk < 4; ++blk) {
+              const int n = n0 + wn * 64 + ni * 32 + blk * 8 + khalf * 4;
+              if (n < N) {
+                f32x4 v;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[q] = acc[mi][ni][blk * 4 + q];
+                *reinterpret_cast<f32x4*>(prow + n) = v;
+              }
+            }
+          }
         } else {
 #pragma unroll
           for (int ni = 0; ni < 2; ++ni) {
@@ -316,6 +347,33 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
         }
       }
     }
+  }
+}
+
+// y[i] = bf16(sum over pieces s of partial[s][i]), pieces in order; 8 outputs per thread.
+__global__ __launch_bounds__(256) void ksplit_reduce_kernel(const float* __restrict__ partial,
+                                                           int64_t count, int ksplit,
+                                                           uint16_t* __restrict__ out) {
+  const int64_t n8 = count / 8;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n8;
+       i += int64_t(gridDim.x) * blockDim.x) {
+    float acc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int s = 0; s < ksplit; ++s) {
+      const f32x4* src = reinterpret_cast<const f32x4*>(partial + s * count) + 2 * i;
+      const f32x4 a = __builtin_nontemporal_load(src);
+      const f32x4 b = __builtin_nontemporal_load(src + 1);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[q] += a[q];
+        acc[4 + q] += b[q];
+      }
+    }
+    u32x4 pk;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) pk[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
+    reinterpret_cast<u32x4*>(out)[i] = pk;
   }
 }
 
@@ -414,17 +472,26 @@ int grid_for(int64_t upper_tiles, int num_cu) {
 hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64_t R, int E, int H,
                            int F, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                            uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint16_t* h,
-                           int num_cu, hipStream_t s) {
+                           float* partial, int ksplit, int num_cu, hipStream_t s) {
   MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix,
              queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
-  GemmArgs a1{queues, x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + 127) / 128};
+  GemmArgs a1{queues, x_perm, wg, wu, h, nullptr, offsets, mtile_prefix, E, H, F, (F + 127) / 128,
+              int(R), 1};
   MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_bf16_kernel<true>,
              dim3(grid_for(mtiles_upper * a1.ntiles, num_cu)), dim3(kGemmThreads), s, a1);
-  GemmArgs a2{queues + 1, h, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + 255) / 256};
+  GemmArgs a2{queues + 1, h, wd, nullptr, y_perm, partial, offsets, mtile_prefix, E, F, H,
+              (H + 255) / 256, int(R), ksplit};
   MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_bf16_kernel<false>,
-             dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)), dim3(kGemmThreads), s, a2);
+             dim3(grid_for(mtiles_upper * a2.ntiles * ksplit, num_cu)), dim3(kGemmThreads), s, a2);
+  if (ksplit > 1) {
+    const int64_t count = R * H;
+    const int64_t threads = count / 8;
+    const unsigned blocks = unsigned(std::min<int64_t>((threads + 255) / 256, int64_t(num_cu) * 16));
+    MOE_LAUNCH("ffn_ksplit_reduce", ksplit_reduce_kernel, dim3(blocks), dim3(256), s, partial, count,
+               ksplit, y_perm);
+  }
   return hipGetLastError();
 }
 

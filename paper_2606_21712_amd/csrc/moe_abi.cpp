@@ -120,12 +120,15 @@ moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, in
   hipError_t err;
   const int ncu = cu_count(&err);
   if (err != hipSuccess) return hip_status("moe_grouped_ffn", err);
+  const int ksplit = moe::ffn_down_ksplit(R, E, H, F, dt);
+  auto* partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + moe::ffn_partial_offset(R, E, F, dt));
   return hip_status(
       "moe_grouped_ffn",
       moe::launch_ffn_bf16(static_cast<const uint16_t*>(x_perm), expert_offsets, R, E, H, F,
                            static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
                            static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm),
-                           prefix, queues, static_cast<uint16_t*>(h), ncu, stream_of(stream)));
+                           prefix, queues, static_cast<uint16_t*>(h), partial, ksplit, ncu,
+                           stream_of(stream)));
 }
 
 moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float* topk_weights,

@@ -19,9 +19,12 @@ struct Check {
 // Workspace layouts (bytes).  Offsets inside the workspace are 256-byte aligned.
 size_t permute_workspace_bytes(int64_t T, int32_t E, int32_t k);
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt);
-// ffn workspace: [m-tile prefix (E + 1 ints) | tile queues (16 ints) | h [R, F]]
+// ffn workspace: [m-tile prefix (E + 1 ints) | tile queues | h [R, F] |
+//                 down-projection partials [ksplit, R, H] fp32 when ksplit > 1]
 size_t ffn_queue_offset(int32_t E);
 size_t ffn_h_offset(int32_t E);
+size_t ffn_partial_offset(int64_t R, int32_t E, int32_t F, moe_dtype dt);
+int ffn_down_ksplit(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt);
 int64_t permute_units(int64_t R);           // count-units (1024 assignments each)
 
 constexpr int64_t kPermuteUnit = 1024;      // assignments per counting unit (one wavefront)

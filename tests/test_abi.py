@@ -99,6 +99,10 @@ def test_ffn_validation(L):
     assert ffn(L, R=0, xp=None, off=None, wg=None, wu=None, wd=None, yp=None, ws=None, ws_bytes=0) == 0
     # fp32 h is twice as large
     assert L.moe_grouped_ffn_workspace_bytes(100, 8, 128, 256, 0) > need
+    # few output tiles with a long k: room for two fp32 partials of the down projection
+    R, H, F = 2048, 256, 4096
+    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, F, 1) >= R * F * 2 + 2 * R * H * 4
+    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, 1024, 1) < R * 1024 * 2 + R * H * 4
 
 
 def combine(L, yp=P, dest=P, w=P, ys=None, T=16, k=2, H=64, dt=1, y=P):

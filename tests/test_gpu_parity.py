@@ -37,6 +37,8 @@ CASES = {
     "k_eq_E": small("k_eq_E", T=260, H=64, E=4, k=4, F=64, seed=17),
     "T1": small("T1", T=1, H=64, E=8, k=2, F=64, seed=18),
     "H64_f32": small("H64_f32", T=333, H=64, E=5, k=2, F=64, seed=19, dtype="f32"),
+    # few down-projection tiles and a long k: the down projection splits k in two
+    "ksplit_small": small("ksplit_small", T=1024, H=256, E=8, k=2, F=4096, seed=20),
 }
 
 
