@@ -104,6 +104,71 @@ def copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes": nbytes, "ms": ms, "GBps_read_plus_write": 2 * nbytes / ms / 1e6}))
 
 
+SWEEP_SHAPES = {
+    # layer shape -> (workload whose weights and routing recipe it uses, largest T)
+    "mixtral": ("mixtral4k", 65536),
+    "deepseek": ("deepseek", 32768),
+    "memconstrained": ("memconstrained", 131072),
+}
+
+
+def expert_batch_sweep(shape: str, steps: int, warmup: int):
+    """Module-level roofline of the MoE layer: time one layer over expert batches of
+    T = 256 .. T_max tokens (the leading T tokens of one seeded batch, so every
+    smaller batch is a prefix of the larger ones) and report tokens/s and grouped
+    FFN TFLOP/s per size.  The saturation batch is the smallest T whose FFN
+    throughput reaches 90% of the largest measured."""
+    import torch
+
+    import moegen
+    import paper_2606_21712_amd as moe
+
+    name, tmax = SWEEP_SHAPES[shape]
+    base = moegen.CONFIGS[name]
+    cfg = base.scaled(T=tmax, routing="router") if base.routing != "router" else base.scaled(T=tmax)
+    log(f"sweep {shape}: generating T={cfg.T} H={cfg.H} E={cfg.E} k={cfg.k} F={cfg.F} Fs={cfg.Fs}")
+    I = moegen.make_inputs(cfg)
+    x, logits = to_dev(I.x, torch), to_dev(I.logits, torch)
+    wg, wu, wd = to_dev(I.w_gate, torch), to_dev(I.w_up, torch), to_dev(I.w_down, torch)
+    shared = (to_dev(I.ws_gate, torch), to_dev(I.ws_up, torch), to_dev(I.ws_down, torch)) if cfg.Fs \
+        else (None, None, None)
+    rows = []
+    T = 256
+    while T <= tmax:
+        layer = moe.MoELayer(T, cfg.H, cfg.E, cfg.k, cfg.F, cfg.Fs)
+        xs, ls = x[:T].contiguous(), logits[:T].contiguous()
+
+        def step():
+            layer.run(xs, ls, wg, wu, wd, *shared, renormalize=cfg.renormalize)
+
+        for _ in range(warmup):
+            step()
+        moe.profiler_start(steps * 16 + 16)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(steps):
+            step()
+        ev1.record()
+        torch.cuda.synchronize()
+        moe.profiler_stop()
+        ms = ev0.elapsed_time(ev1) / steps
+        ffn_ms = sum(t for n, t in moe.profiler_records() if n.startswith("ffn_")) / steps
+        flops = 6.0 * cfg.H * cfg.F * T * cfg.k + 6.0 * cfg.H * cfg.Fs * T
+        row = {"tokens": T, "ms_per_layer": round(ms, 4), "tokens_per_s": round(T / ms * 1e3, 1),
+               "ffn_ms": round(ffn_ms, 4), "ffn_tflops": round(flops / ffn_ms / 1e9, 1),
+               "tokens_per_expert": T * cfg.k / cfg.E}
+        rows.append(row)
+        print(json.dumps({"sweep": shape, **row}), flush=True)
+        del layer
+        T *= 2
+    peak = max(r["ffn_tflops"] for r in rows)
+    sat = next(r["tokens"] for r in rows if r["ffn_tflops"] >= 0.9 * peak)
+    print(json.dumps({"sweep": shape, "summary": True, "peak_ffn_tflops": peak,
+                      "saturation_tokens_90pct": sat,
+                      "saturation_tokens_per_expert": sat * cfg.k / cfg.E}), flush=True)
+
+
 def main():
     import moegen
 
@@ -115,9 +180,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
+    ap.add_argument("--sweep", choices=["mixtral", "deepseek", "memconstrained"], default=None,
+                    help="expert-batch sweep of one layer shape: one JSON line per batch size")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.sweep:
+        return expert_batch_sweep(args.sweep, args.steps, args.warmup)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
