@@ -178,6 +178,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="mixtral4k", choices=sorted(moegen.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gather", action="store_true",
+                    help="materialize x_perm in moe_permute instead of gathering rows in the grouped FFN")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
     ap.add_argument("--sweep", choices=["mixtral", "deepseek", "memconstrained"], default=None,
@@ -214,7 +216,7 @@ def main():
     wg, wu, wd = to_dev(I.w_gate, torch), to_dev(I.w_up, torch), to_dev(I.w_down, torch)
     shared = (to_dev(I.ws_gate, torch), to_dev(I.ws_up, torch), to_dev(I.ws_down, torch)) if c.Fs \
         else (None, None, None)
-    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt)
+    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt, gather=not args.no_gather)
     stream = torch.cuda.current_stream()
 
     def step():
@@ -263,7 +265,9 @@ def main():
     b = 4 if c.dtype == "f32" else 2
     bytes_alg = {
         "route": c.T * c.E * 4 + c.T * c.k * 8,
-        "permute": c.T * c.H * b + R * c.H * b + 3 * R * 4,
+        # ids read + dest_rows and sorted_token_ids written (+ x read and x_perm written
+        # when the rows are materialized rather than gathered by the grouped FFN)
+        "permute": 3 * R * 4 + (0 if not args.no_gather else c.T * c.H * b + R * c.H * b),
         "combine": R * c.H * b + c.T * c.H * b * (2 if c.Fs else 1) + c.T * c.k * 8,
     }
     perm_us = sum(kernels[k]["avg_us"] for k in kernels if k.startswith("permute_"))
@@ -288,7 +292,9 @@ def main():
         "dtype": "f32" if c.dtype == "f32" else "bf16",
         "data": "synthetic (seeded generator; random-init expert weights)",
         "config": {"workload": c.name, "tokens": c.T, "hidden": c.H, "experts": c.E, "top_k": c.k,
-                   "ffn_dim": c.F, "shared_ffn_dim": c.Fs, "routing": c.routing, "seed": c.seed},
+                   "ffn_dim": c.F, "shared_ffn_dim": c.Fs, "routing": c.routing, "seed": c.seed,
+                   "path": "permute maps + gather-fused grouped FFN" if not args.no_gather
+                   else "permute with x_perm + grouped FFN"},
         "ffn_tflops": round(ffn_tflops, 1) if ffn_tflops else None,
         "ffn_frac_peak": round(ffn_tflops / peak, 4) if ffn_tflops else None,
         "roofline": {

@@ -105,7 +105,10 @@ moe_status moe_route(const float* logits, int64_t T, int32_t E, int32_t k, int32
  *   expert_offsets    i32 [E + 1]     out: exclusive prefix sum, offsets[E] = T*k
  *   sorted_token_ids  i32 [T*k]       out: source token of each grouped row
  *   dest_rows         i32 [T, k]      out: grouped row of assignment (t, j)
- *   x_perm            dt  [T*k, H]    out: x_perm[r] = x[sorted_token_ids[r]]
+ *   x_perm            dt  [T*k, H]    out: x_perm[r] = x[sorted_token_ids[r]], or NULL:
+ *                                     then only the maps are produced and x is not read
+ *                                     (x may be NULL); moe_grouped_ffn_gather reads the
+ *                                     rows through sorted_token_ids instead
  *   ws, ws_bytes      device scratch of at least moe_permute_workspace_bytes()
  *
  * Expert e owns rows offsets[e] .. offsets[e+1]-1, holding its tokens in
@@ -143,6 +146,27 @@ moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, in
                            int32_t H, int32_t F, const void* w_gate, const void* w_up,
                            const void* w_down, moe_dtype dt, void* y_perm, void* ws,
                            size_t ws_bytes, moe_stream stream);
+
+/*
+ * moe_grouped_ffn_gather - moe_grouped_ffn reading each grouped row straight
+ * from the token rows: row r of group e is x[sorted_token_ids[r]].  The same
+ * result as moe_permute's x_perm followed by moe_grouped_ffn, bit for bit, but
+ * the grouped copy of the activations (T*k rows) is never written or read.
+ *
+ *   x                 dt  [T, H]   token rows (T * H * element size < 2^31)
+ *   sorted_token_ids  i32 [R]      from moe_permute (R = T*k)
+ *   other arguments as moe_grouped_ffn; the workspace size is
+ *   moe_grouped_ffn_workspace_bytes(R, E, H, F, dt)
+ *
+ * Errors: as moe_grouped_ffn, plus INVALID_ARGUMENT for T < 0, R > 0 with
+ * T = 0, a NULL or misaligned x or sorted_token_ids; UNSUPPORTED when x is
+ * 2 GiB or larger.  Token ids are not checked (precondition: 0 <= id < T).
+ */
+moe_status moe_grouped_ffn_gather(const void* x, const int32_t* sorted_token_ids,
+                                  const int32_t* expert_offsets, int64_t T, int64_t R, int32_t E,
+                                  int32_t H, int32_t F, const void* w_gate, const void* w_up,
+                                  const void* w_down, moe_dtype dt, void* y_perm, void* ws,
+                                  size_t ws_bytes, moe_stream stream);
 
 /*
  * moe_combine - gate-weighted sum of each token's k expert outputs (the MoE

@@ -17,7 +17,7 @@ import torch
 
 __all__ = [
     "MoEError", "lib", "LIB_PATH", "HEADER_PATH", "abi_version", "exported_symbols",
-    "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
+    "moe_route", "moe_permute", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
     "profiler_start", "profiler_stop", "profiler_records",
     "DTYPE_F32", "DTYPE_BF16",
@@ -56,6 +56,8 @@ _SIGNATURES = {
     "moe_grouped_ffn_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I32, ctypes.c_int]),
     "moe_grouped_ffn": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, ctypes.c_int, _P,
                                        _P, _SZ, _P]),
+    "moe_grouped_ffn_gather": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P,
+                                              ctypes.c_int, _P, _P, _SZ, _P]),
     "moe_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I32, _I32, ctypes.c_int, _P, _P]),
     "moe_profiler_start": (ctypes.c_int, [ctypes.c_int]),
     "moe_profiler_stop": (ctypes.c_int, []),
@@ -143,8 +145,9 @@ def moe_permute_workspace_bytes(T, E, k) -> int:
     return lib().moe_permute_workspace_bytes(T, E, k)
 
 
-def moe_permute(topk_ids, x, E, out=None, ws=None, stream=None):
-    """-> dict(counts, offsets, sorted_token_ids, dest_rows, x_perm)."""
+def moe_permute(topk_ids, x, E, out=None, ws=None, stream=None, gather_rows=True):
+    """-> dict(counts, offsets, sorted_token_ids, dest_rows, x_perm).  With
+    gather_rows=False (or out["x_perm"] None) only the maps are produced."""
     T, k = topk_ids.shape
     H = x.shape[1]
     dev = x.device
@@ -153,7 +156,7 @@ def moe_permute(topk_ids, x, E, out=None, ws=None, stream=None):
                    offsets=torch.empty(E + 1, dtype=torch.int32, device=dev),
                    sorted_token_ids=torch.empty(T * k, dtype=torch.int32, device=dev),
                    dest_rows=torch.empty((T, k), dtype=torch.int32, device=dev),
-                   x_perm=torch.empty((T * k, H), dtype=x.dtype, device=dev))
+                   x_perm=torch.empty((T * k, H), dtype=x.dtype, device=dev) if gather_rows else None)
     if ws is None:
         ws = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), dtype=torch.uint8, device=dev)
     _dev(topk_ids, x, ws, *out.values())
@@ -184,6 +187,28 @@ def moe_grouped_ffn(x_perm, offsets, w_gate, w_up, w_down, y_perm=None, ws=None,
     _check(lib().moe_grouped_ffn(_ptr(x_perm), _ptr(offsets), R, E, H, F, _ptr(w_gate), _ptr(w_up),
                                  _ptr(w_down), _dt(x_perm), _ptr(y_perm), _ptr(ws), ws.numel(),
                                  _stream(stream, dev)))
+    return y_perm
+
+
+def moe_grouped_ffn_gather(x, sorted_token_ids, offsets, w_gate, w_up, w_down, y_perm=None, ws=None,
+                           stream=None):
+    """Grouped FFN reading row r of the groups from x[sorted_token_ids[r]] -> y_perm [R, H]."""
+    T, H = x.shape
+    R = sorted_token_ids.shape[0]
+    E, F, _ = w_gate.shape
+    dev = x.device
+    if y_perm is None:
+        y_perm = torch.empty((R, H), dtype=x.dtype, device=dev)
+    if ws is None:
+        ws = torch.empty(max(1, moe_grouped_ffn_workspace_bytes(R, E, H, F, x.dtype)),
+                         dtype=torch.uint8, device=dev)
+    _dev(x, sorted_token_ids, offsets, w_gate, w_up, w_down, y_perm, ws)
+    for w in (w_gate, w_up, w_down):
+        if w.dtype != x.dtype:
+            raise TypeError("weights and activations must share a dtype")
+    _check(lib().moe_grouped_ffn_gather(_ptr(x), _ptr(sorted_token_ids), _ptr(offsets), T, R, E, H, F,
+                                        _ptr(w_gate), _ptr(w_up), _ptr(w_down), _dt(x), _ptr(y_perm),
+                                        _ptr(ws), ws.numel(), _stream(stream, dev)))
     return y_perm
 
 
@@ -224,11 +249,16 @@ def profiler_records():
 # --------------------------------------------------------------------------- whole layer
 class MoELayer:
     """Preallocated buffers for one layer shape; ``run`` issues the calls on one stream
-    with no allocation and no host synchronization."""
+    with no allocation and no host synchronization.
 
-    def __init__(self, T, H, E, k, F, Fs=0, dtype=torch.bfloat16, device="cuda"):
+    gather=False: route, permute (with x_perm), grouped FFN, combine.
+    gather=True:  route, permute (maps only), grouped FFN gathering the token rows,
+                  combine -- the same output without the grouped copy of x."""
+
+    def __init__(self, T, H, E, k, F, Fs=0, dtype=torch.bfloat16, device="cuda", gather=False):
         self.T, self.H, self.E, self.k, self.F, self.Fs = T, H, E, k, F, Fs
         self.dtype = dtype
+        self.gather = gather
         dev = torch.device(device)
         R = T * k
         i32 = dict(dtype=torch.int32, device=dev)
@@ -236,7 +266,7 @@ class MoELayer:
         self.topk_weights = torch.empty((T, k), dtype=torch.float32, device=dev)
         self.perm = dict(counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32),
                          sorted_token_ids=torch.empty(R, **i32), dest_rows=torch.empty((T, k), **i32),
-                         x_perm=torch.empty((R, H), dtype=dtype, device=dev))
+                         x_perm=None if gather else torch.empty((R, H), dtype=dtype, device=dev))
         self.ws_perm = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), dtype=torch.uint8, device=dev)
         self.y_perm = torch.empty((R, H), dtype=dtype, device=dev)
         self.ws_ffn = torch.empty(max(1, moe_grouped_ffn_workspace_bytes(R, E, H, F, dtype)),
@@ -254,8 +284,12 @@ class MoELayer:
             renormalize=1, stream=None):
         moe_route(logits, self.k, renormalize, self.topk_ids, self.topk_weights, stream=stream)
         moe_permute(self.topk_ids, x, self.E, out=self.perm, ws=self.ws_perm, stream=stream)
-        moe_grouped_ffn(self.perm["x_perm"], self.perm["offsets"], w_gate, w_up, w_down,
-                        y_perm=self.y_perm, ws=self.ws_ffn, stream=stream)
+        if self.gather:
+            moe_grouped_ffn_gather(x, self.perm["sorted_token_ids"], self.perm["offsets"], w_gate, w_up,
+                                   w_down, y_perm=self.y_perm, ws=self.ws_ffn, stream=stream)
+        else:
+            moe_grouped_ffn(self.perm["x_perm"], self.perm["offsets"], w_gate, w_up, w_down,
+                            y_perm=self.y_perm, ws=self.ws_ffn, stream=stream)
         if self.Fs:
             moe_grouped_ffn(x, self.shared_offsets, ws_gate, ws_up, ws_down, y_perm=self.y_shared,
                             ws=self.ws_shared, stream=stream)

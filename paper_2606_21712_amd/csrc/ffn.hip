@@ -80,7 +80,8 @@ constexpr int kGroupM = 4;
 
 struct GemmArgs {
   int32_t* queue;                 // tile counter, zeroed by tile_prefix_kernel
-  const uint16_t* act;            // [R, K]
+  const uint16_t* act;            // [R, K]; with a gather, the token rows [T, K]
+  const int32_t* gather;          // [R] token of each grouped row (gather only)
   const uint16_t* w0;             // [E, N, K] (GEMM-1: W_gate; GEMM-2: W_down)
   const uint16_t* w1;             // [E, N, K] (GEMM-1: W_up)
   uint16_t* out;                  // [R, N]
@@ -88,6 +89,7 @@ struct GemmArgs {
   const int32_t* offsets;         // [E + 1]
   const int32_t* mtile_prefix;    // [E + 1]
   int E, K, N, ntiles, R, ksplit;
+  int act_bytes;                  // bytes of act (gather only; < 2^31)
 };
 
 // First tile row of a wavefront's n-subtile ni (0..1).  GEMM-1: ni = 0 is 32
@@ -109,7 +111,9 @@ constexpr int kWaitVm0 = 0x0F70;
 // Buffer resource word 3 for raw (unformatted, stride 0) buffer loads on gfx9.
 constexpr int kBufFlags = 0x00020000;
 
-template <bool SWIGLU>
+// GATHER: activation row r of the tile list is row gather[r] of act (the token
+// rows themselves), so the grouped copy of the activations is never written.
+template <bool SWIGLU, bool GATHER>
 __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(GemmArgs p) {
   // Two pipeline stages, each [weight tile | activation tile].  They are filled by
   // direct global->LDS loads; two distinct objects let the compiler tell them apart.
@@ -192,8 +196,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     const int n0 = SWIGLU ? nt * 128 : nt * 256;
     const int wrows = SWIGLU ? min(128, N - n0) : min(256, N - n0);
     const int64_t rowb = int64_t(K) * 2;
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(p.act) + int64_t(row0) * K, 0, int(arows * rowb), kBufFlags);
+    const __amdgpu_buffer_rsrc_t ra =
+        GATHER ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.act), 0, p.act_bytes, kBufFlags)
+               : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.act) + int64_t(row0) * K, 0,
+                                                   int(arows * rowb), kBufFlags);
     const int64_t wfirst = (int64_t(e) * N + n0) * K;
     const __amdgpu_buffer_rsrc_t rw0 = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
@@ -205,7 +211,13 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     for (int i = 0; i < 4; ++i) {
       const int r = (8 * i + wave) * 8 + qrow;                  // tile row this lane fills
       const uint32_t cb = uint32_t(swz(r, qpos) * 16);          // its logical chunk, in bytes
-      aoff[i] = uint32_t(r) * uint32_t(rowb) + cb;
+      if (GATHER) {
+        // The token's row; rows past the group end get an offset beyond num_records.
+        const int grow = row0 + r;
+        aoff[i] = grow < row_end ? uint32_t(p.gather[grow]) * uint32_t(rowb) + cb : 0x80000000u;
+      } else {
+        aoff[i] = uint32_t(r) * uint32_t(rowb) + cb;
+      }
       // GEMM-1: tile rows 0..127 are gate features n0.., rows 128..255 the same up features.
       woff[i] = uint32_t(SWIGLU ? (r & 127) : r) * uint32_t(rowb) + cb;
     }
@@ -384,6 +396,7 @@ constexpr int kFM = 64, kFN = 64, kFK = 16;
 
 struct GemmArgsF {
   const float* act;
+  const int32_t* gather;          // [R] token of each grouped row, or null
   const float* w0;
   const float* w1;
   float* out;
@@ -414,7 +427,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_f32_kernel(GemmArgsF p) {
   const float* wu = SWIGLU ? p.w1 + int64_t(e) * N * K : nullptr;
   const int tx = tid & 15, ty = tid >> 4;
   const int lrow = tid >> 2, lk = (tid & 3) * 4;               // loader: one float4 per thread
-  const int64_t arow = min(row0 + lrow, row_end - 1);
+  const int64_t arow = p.gather != nullptr ? int64_t(p.gather[min(row0 + lrow, row_end - 1)])
+                                           : int64_t(min(row0 + lrow, row_end - 1));
   const int64_t wrow = min(n0 + lrow, N - 1);
   float ag[4][4] = {}, au[4][4] = {};
   for (int k0 = 0; k0 < K; k0 += kFK) {
@@ -469,21 +483,24 @@ int grid_for(int64_t upper_tiles, int num_cu) {
 
 }  // namespace
 
-hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64_t R, int E, int H,
-                           int F, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
-                           uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint16_t* h,
-                           float* partial, int ksplit, int num_cu, hipStream_t s) {
+hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T, const int32_t* offsets,
+                           int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
+                           const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
+                           uint16_t* h, float* partial, int ksplit, int num_cu, hipStream_t s) {
   MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix,
              queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
-  GemmArgs a1{queues, x_perm, wg, wu, h, nullptr, offsets, mtile_prefix, E, H, F, (F + 127) / 128,
-              int(R), 1};
-  MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_bf16_kernel<true>,
-             dim3(grid_for(mtiles_upper * a1.ntiles, num_cu)), dim3(kGemmThreads), s, a1);
-  GemmArgs a2{queues + 1, h, wd, nullptr, y_perm, partial, offsets, mtile_prefix, E, F, H,
-              (H + 255) / 256, int(R), ksplit};
-  MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_bf16_kernel<false>,
+  GemmArgs a1{queues, act, gather, wg, wu, h, nullptr, offsets, mtile_prefix, E, H, F, (F + 127) / 128,
+              int(R), 1, int(T * H * 2)};
+  const dim3 grid1(grid_for(mtiles_upper * a1.ntiles, num_cu));
+  if (gather != nullptr)
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, true>), grid1, dim3(kGemmThreads), s, a1);
+  else
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, false>), grid1, dim3(kGemmThreads), s, a1);
+  GemmArgs a2{queues + 1, h, nullptr, wd, nullptr, y_perm, partial, offsets, mtile_prefix, E, F, H,
+              (H + 255) / 256, int(R), ksplit, 0};
+  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_bf16_kernel<false, false>),
              dim3(grid_for(mtiles_upper * a2.ntiles * ksplit, num_cu)), dim3(kGemmThreads), s, a2);
   if (ksplit > 1) {
     const int64_t count = R * H;
@@ -495,16 +512,16 @@ hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64
   return hipGetLastError();
 }
 
-hipError_t launch_ffn_f32(const float* x_perm, const int32_t* offsets, int64_t R, int E, int H, int F,
-                          const float* wg, const float* wu, const float* wd, float* y_perm,
-                          int32_t* mtile_prefix, float* h, hipStream_t s) {
+hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
+                          int E, int H, int F, const float* wg, const float* wu, const float* wd,
+                          float* y_perm, int32_t* mtile_prefix, float* h, hipStream_t s) {
   MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, mtile_prefix,
              static_cast<int32_t*>(nullptr));
   const int64_t mtiles_upper = (R + int64_t(E) * (kFM - 1)) / kFM;
-  GemmArgsF a1{x_perm, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + kFN - 1) / kFN};
+  GemmArgsF a1{act, gather, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + kFN - 1) / kFN};
   MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_f32_kernel<true>, dim3(unsigned(mtiles_upper * a1.ntiles)),
              dim3(256), s, a1);
-  GemmArgsF a2{h, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + kFN - 1) / kFN};
+  GemmArgsF a2{h, nullptr, wd, nullptr, y_perm, offsets, mtile_prefix, E, F, H, (H + kFN - 1) / kFN};
   MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_f32_kernel<false>, dim3(unsigned(mtiles_upper * a2.ntiles)),
              dim3(256), s, a2);
   return hipGetLastError();

@@ -99,6 +99,36 @@ size_t moe_grouped_ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t 
   return moe::ffn_workspace_bytes(R, E, H, F, dt);
 }
 
+namespace {
+
+moe_status run_ffn(const char* fn, const void* act, const int32_t* gather, int64_t T,
+                   const int32_t* expert_offsets, int64_t R, int32_t E, int32_t H, int32_t F,
+                   const void* w_gate, const void* w_up, const void* w_down, moe_dtype dt, void* y_perm,
+                   void* ws, moe_stream stream) {
+  auto* prefix = static_cast<int32_t*>(ws);
+  auto* queues = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(ws) + moe::ffn_queue_offset(E));
+  void* h = static_cast<uint8_t*>(ws) + moe::ffn_h_offset(E);
+  if (dt == MOE_DTYPE_F32) {
+    return hip_status(fn, moe::launch_ffn_f32(static_cast<const float*>(act), gather, expert_offsets, R, E,
+                                              H, F, static_cast<const float*>(w_gate),
+                                              static_cast<const float*>(w_up),
+                                              static_cast<const float*>(w_down), static_cast<float*>(y_perm),
+                                              prefix, static_cast<float*>(h), stream_of(stream)));
+  }
+  hipError_t err;
+  const int ncu = cu_count(&err);
+  if (err != hipSuccess) return hip_status(fn, err);
+  const int ksplit = moe::ffn_down_ksplit(R, E, H, F, dt);
+  auto* partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + moe::ffn_partial_offset(R, E, F, dt));
+  return hip_status(
+      fn, moe::launch_ffn_bf16(static_cast<const uint16_t*>(act), gather, T, expert_offsets, R, E, H, F,
+                               static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
+                               static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), prefix,
+                               queues, static_cast<uint16_t*>(h), partial, ksplit, ncu, stream_of(stream)));
+}
+
+}  // namespace
+
 moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, int64_t R, int32_t E,
                            int32_t H, int32_t F, const void* w_gate, const void* w_up,
                            const void* w_down, moe_dtype dt, void* y_perm, void* ws,
@@ -106,29 +136,20 @@ moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, in
   moe::Check c = moe::validate_ffn(x_perm, expert_offsets, R, E, H, F, w_gate, w_up, w_down, dt,
                                    y_perm, ws, ws_bytes);
   if (!c.ok() || R == 0) return finish(c);
-  auto* prefix = static_cast<int32_t*>(ws);
-  auto* queues = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(ws) + moe::ffn_queue_offset(E));
-  void* h = static_cast<uint8_t*>(ws) + moe::ffn_h_offset(E);
-  if (dt == MOE_DTYPE_F32) {
-    return hip_status(
-        "moe_grouped_ffn",
-        moe::launch_ffn_f32(static_cast<const float*>(x_perm), expert_offsets, R, E, H, F,
-                            static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
-                            static_cast<const float*>(w_down), static_cast<float*>(y_perm), prefix,
-                            static_cast<float*>(h), stream_of(stream)));
-  }
-  hipError_t err;
-  const int ncu = cu_count(&err);
-  if (err != hipSuccess) return hip_status("moe_grouped_ffn", err);
-  const int ksplit = moe::ffn_down_ksplit(R, E, H, F, dt);
-  auto* partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + moe::ffn_partial_offset(R, E, F, dt));
-  return hip_status(
-      "moe_grouped_ffn",
-      moe::launch_ffn_bf16(static_cast<const uint16_t*>(x_perm), expert_offsets, R, E, H, F,
-                           static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
-                           static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm),
-                           prefix, queues, static_cast<uint16_t*>(h), partial, ksplit, ncu,
-                           stream_of(stream)));
+  return run_ffn("moe_grouped_ffn", x_perm, nullptr, R, expert_offsets, R, E, H, F, w_gate, w_up, w_down,
+                 dt, y_perm, ws, stream);
+}
+
+moe_status moe_grouped_ffn_gather(const void* x, const int32_t* sorted_token_ids,
+                                  const int32_t* expert_offsets, int64_t T, int64_t R, int32_t E,
+                                  int32_t H, int32_t F, const void* w_gate, const void* w_up,
+                                  const void* w_down, moe_dtype dt, void* y_perm, void* ws,
+                                  size_t ws_bytes, moe_stream stream) {
+  moe::Check c = moe::validate_ffn_gather(x, sorted_token_ids, T, expert_offsets, R, E, H, F, w_gate,
+                                          w_up, w_down, dt, y_perm, ws, ws_bytes);
+  if (!c.ok() || R == 0) return finish(c);
+  return run_ffn("moe_grouped_ffn_gather", x, sorted_token_ids, T, expert_offsets, R, E, H, F, w_gate,
+                 w_up, w_down, dt, y_perm, ws, stream);
 }
 
 moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float* topk_weights,

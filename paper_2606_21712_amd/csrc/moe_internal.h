@@ -29,16 +29,17 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
                           int32_t* counts, int32_t* offsets, int32_t* sorted_tok, int32_t* dest,
                           void* x_perm, int32_t* unit_counts, int64_t units_padded, hipStream_t s);
 
-// Grouped SwiGLU FFN (bf16).  Device scratch: mtile_prefix (E + 1 ints), queues
-// (2 ints), h [R, F], and partial [ksplit, R, H] fp32 when ksplit > 1; all are
-// rewritten by the call before use.
-hipError_t launch_ffn_bf16(const uint16_t* x_perm, const int32_t* offsets, int64_t R, int E, int H,
-                           int F, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
-                           uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint16_t* h,
-                           float* partial, int ksplit, int num_cu, hipStream_t s);
-hipError_t launch_ffn_f32(const float* x_perm, const int32_t* offsets, int64_t R, int E, int H, int F,
-                          const float* wg, const float* wu, const float* wd, float* y_perm,
-                          int32_t* mtile_prefix, float* h, hipStream_t s);
+// Grouped SwiGLU FFN (bf16).  act is x_perm [R, H], or with gather != null the
+// token rows x [T, H] read through gather[r] (T * H * 2 < 2^31).  Device scratch:
+// mtile_prefix (E + 1 ints), queues (2 ints), h [R, F], and partial [ksplit, R, H]
+// fp32 when ksplit > 1; all are rewritten by the call before use.
+hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T, const int32_t* offsets,
+                           int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
+                           const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
+                           uint16_t* h, float* partial, int ksplit, int num_cu, hipStream_t s);
+hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
+                          int E, int H, int F, const float* wg, const float* wu, const float* wd,
+                          float* y_perm, int32_t* mtile_prefix, float* h, hipStream_t s);
 
 hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                           int64_t T, int k, int H, bool bf16, void* y, hipStream_t s);

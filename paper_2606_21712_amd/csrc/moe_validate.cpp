@@ -137,10 +137,12 @@ Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, 
   MOE_TRY(ptr(fn, "expert_counts", counts));
   MOE_TRY(ptr(fn, "expert_offsets", offsets));
   MOE_TRY(ptr(fn, "topk_ids", ids));
-  MOE_TRY(ptr(fn, "x", x));
   MOE_TRY(ptr(fn, "sorted_token_ids", sorted_tok));
   MOE_TRY(ptr(fn, "dest_rows", dest));
-  MOE_TRY(ptr(fn, "x_perm", x_perm));
+  if (x_perm != nullptr) {            // x_perm NULL: only the maps are produced, x is not read
+    MOE_TRY(ptr(fn, "x", x));
+    MOE_TRY(ptr(fn, "x_perm", x_perm));
+  }
   size_t need = permute_workspace_bytes(T, E, k);
   if (ws_bytes < need)
     return fail(MOE_ERR_WORKSPACE_TOO_SMALL, fn, "workspace %lld bytes < %lld needed",
@@ -149,10 +151,12 @@ Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, 
   return Check{};
 }
 
-Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
-                   int32_t F, const void* wg, const void* wu, const void* wd, int dt,
-                   const void* y_perm, const void* ws, size_t ws_bytes) {
-  const char* fn = "moe_grouped_ffn";
+namespace {
+
+// Checks shared by both grouped-FFN entry points; `act` is x_perm or x.
+Check ffn_common(const char* fn, const char* act_name, const void* act, const int32_t* offsets, int64_t R,
+                 int32_t E, int32_t H, int32_t F, const void* wg, const void* wu, const void* wd, int dt,
+                 const void* y_perm, const void* ws, size_t ws_bytes) {
   if (E < 1) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "E=%lld must be >= 1", E);
   if (E > MOE_MAX_EXPERTS) return fail(MOE_ERR_UNSUPPORTED, fn, "E=%lld exceeds %lld", E, MOE_MAX_EXPERTS);
   if (R < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "R=%lld is negative", R);
@@ -164,7 +168,7 @@ Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_
   if (int64_t(H) * int64_t(F) * int64_t(elt(dt)) >= (int64_t(1) << 31) || H > (1 << 20) || F > (1 << 20))
     return fail(MOE_ERR_UNSUPPORTED, fn, "H=%lld x F=%lld expert matrix exceeds 2 GiB", H, F);
   if (R == 0) return Check{};
-  MOE_TRY(ptr(fn, "x_perm", x_perm));
+  MOE_TRY(ptr(fn, act_name, act));
   MOE_TRY(ptr(fn, "expert_offsets", offsets));
   MOE_TRY(ptr(fn, "w_gate", wg));
   MOE_TRY(ptr(fn, "w_up", wu));
@@ -175,6 +179,30 @@ Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_
     return fail(MOE_ERR_WORKSPACE_TOO_SMALL, fn, "workspace %lld bytes < %lld needed",
                 (long long)ws_bytes, (long long)need);
   MOE_TRY(ptr(fn, "ws", ws));
+  return Check{};
+}
+
+}  // namespace
+
+Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
+                   int32_t F, const void* wg, const void* wu, const void* wd, int dt,
+                   const void* y_perm, const void* ws, size_t ws_bytes) {
+  return ffn_common("moe_grouped_ffn", "x_perm", x_perm, offsets, R, E, H, F, wg, wu, wd, dt, y_perm, ws,
+                    ws_bytes);
+}
+
+Check validate_ffn_gather(const void* x, const int32_t* sorted_tok, int64_t T, const int32_t* offsets,
+                          int64_t R, int32_t E, int32_t H, int32_t F, const void* wg, const void* wu,
+                          const void* wd, int dt, const void* y_perm, const void* ws, size_t ws_bytes) {
+  const char* fn = "moe_grouped_ffn_gather";
+  if (T < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "T=%lld is negative", T);
+  if (R > 0 && T == 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "R=%lld rows but T=0 tokens", R);
+  MOE_TRY(ffn_common(fn, "x", x, offsets, R, E, H, F, wg, wu, wd, dt, y_perm, ws, ws_bytes));
+  if (R == 0) return Check{};
+  // The gathered rows are addressed with 32-bit byte offsets into x.
+  if (T * int64_t(H) * int64_t(elt(dt)) >= (int64_t(1) << 31))
+    return fail(MOE_ERR_UNSUPPORTED, fn, "x of T=%lld rows exceeds 2 GiB for the gather", T);
+  MOE_TRY(ptr(fn, "sorted_token_ids", sorted_tok));
   return Check{};
 }
 

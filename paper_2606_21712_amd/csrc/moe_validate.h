@@ -37,6 +37,9 @@ Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, 
 Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
                    int32_t F, const void* wg, const void* wu, const void* wd, int dt,
                    const void* y_perm, const void* ws, size_t ws_bytes);
+Check validate_ffn_gather(const void* x, const int32_t* sorted_tok, int64_t T, const int32_t* offsets,
+                          int64_t R, int32_t E, int32_t H, int32_t F, const void* wg, const void* wu,
+                          const void* wd, int dt, const void* y_perm, const void* ws, size_t ws_bytes);
 Check validate_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                        int64_t T, int32_t k, int32_t H, int dt, const void* y);
 

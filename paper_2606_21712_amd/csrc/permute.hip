@@ -162,6 +162,7 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
   MOE_LAUNCH("permute_scan", permute_scan_kernel, dim3(E), dim3(kThreads), s, uc, U, Upad, counts);
   MOE_LAUNCH("permute_rank", permute_rank_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E, k,
              nbits, Upad, uc, counts, offsets, dest, sorted_tok);
+  if (x_perm == nullptr) return hipGetLastError();     // maps only: the grouped FFN gathers rows
   const int64_t row_bytes = int64_t(H) * elt;
   const unsigned copy_blocks = unsigned((T + kWavesPerBlock - 1) / kWavesPerBlock);
   MOE_LAUNCH("permute_copy", permute_copy_kernel<4>, dim3(copy_blocks), dim3(kThreads), s,

@@ -105,6 +105,31 @@ def test_ffn_validation(L):
     assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, 1024, 1) < R * 1024 * 2 + R * H * 4
 
 
+def ffn_gather(L, x=P, st=P, off=P, T=50, R=100, E=8, H=128, F=256, wg=P, wu=P, wd=P, dt=1, yp=P, ws=P,
+               ws_bytes=1 << 30):
+    return L.moe_grouped_ffn_gather(x, st, off, T, R, E, H, F, wg, wu, wd, dt, yp, ws, ws_bytes, S)
+
+
+def test_ffn_gather_validation(L):
+    assert ffn_gather(L, st=None) == INVALID
+    assert b"sorted_token_ids" in L.moe_last_error()
+    assert ffn_gather(L, x=None) == INVALID
+    assert b"x is NULL" in L.moe_last_error()
+    assert ffn_gather(L, T=0) == INVALID
+    assert ffn_gather(L, T=-1) == INVALID
+    assert ffn_gather(L, T=2**20, H=1024) == UNSUPPORTED           # x of 2 GiB
+    assert ffn_gather(L, ws_bytes=10) == WS_SMALL
+    assert ffn_gather(L, R=0, T=0, x=None, st=None, off=None, wg=None, wu=None, wd=None, yp=None,
+                      ws=None, ws_bytes=0) == 0
+
+
+def test_permute_maps_only_needs_no_rows(L):
+    # x_perm NULL: x may be NULL too; validation passes up to the launch.  T = 0 keeps it a no-op.
+    assert permute(L, T=0, x=None, xp=None, ids=None, cnt=None, off=None, st=None, dest=None, ws=None,
+                   ws_bytes=0) == 0
+    assert permute(L, x=None, xp=P) == INVALID
+
+
 def combine(L, yp=P, dest=P, w=P, ys=None, T=16, k=2, H=64, dt=1, y=P):
     return L.moe_combine(yp, dest, w, ys, T, k, H, dt, y, S)
 

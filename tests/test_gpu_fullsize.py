@@ -85,3 +85,14 @@ def test_full_size_layer(name):
     err = rel_max_err(y_g, y_ref)
     log(f"[gpu] full-size {name}: max|dy|/max|y| = {err:.3e}")
     assert err <= BF16_TOL
+
+    # the gather-fused grouped FFN reproduces the same layer bit for bit
+    log(f"[gpu] full-size {name}: gather-fused path")
+    y_first, yp_first = layer.y.clone(), layer.y_perm.clone()
+    del layer
+    g = moe.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.F, cfg.Fs, gather=True)
+    g.run(to_dev(I.x), to_dev(I.logits), to_dev(I.w_gate), to_dev(I.w_up), to_dev(I.w_down),
+          *shared_dev, renormalize=cfg.renormalize)
+    torch.cuda.synchronize()
+    assert torch.equal(g.y_perm, yp_first)
+    assert torch.equal(g.y, y_first)

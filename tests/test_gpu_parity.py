@@ -51,17 +51,17 @@ def inputs(name):
     return _INPUTS[name]
 
 
-def run_layer(I, renormalize=1):
+def run_layer(I, renormalize=1, gather=False):
     c = I.cfg
     dt = torch.float32 if c.dtype == "f32" else torch.bfloat16
-    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt)
+    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt, gather=gather)
     shared = (to_dev(I.ws_gate), to_dev(I.ws_up), to_dev(I.ws_down)) if c.Fs else (None, None, None)
     layer.run(to_dev(I.x), to_dev(I.logits), to_dev(I.w_gate), to_dev(I.w_up), to_dev(I.w_down),
               *shared, renormalize=renormalize)
     torch.cuda.synchronize()
     out = dict(ids=to_host(layer.topk_ids), w=to_host(layer.topk_weights),
                y_perm=to_host(layer.y_perm), y=to_host(layer.y))
-    out.update({k: to_host(v) for k, v in layer.perm.items()})
+    out.update({k: to_host(v) for k, v in layer.perm.items() if v is not None})
     if c.Fs:
         out["y_shared"] = to_host(layer.y_shared)
     return out
@@ -99,6 +99,22 @@ def test_layer_parity(name):
     err = rel_max_err(f64(g["y"]), o["y"])
     log(f"[gpu]   max|dy|/max|y| = {err:.3e}")
     assert err <= tol
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "mixtral_small", "zipf_small", "deepseek_small", "memc_small",
+                                  "uniform_router", "T1", "ksplit_small", "H64_f32"])
+def test_gather_path_matches_grouped_path(name):
+    """moe_grouped_ffn_gather gives bit-for-bit the y_perm of moe_grouped_ffn on x_perm,
+    and the layer output stays within the oracle bar."""
+    I = inputs(name)
+    c = I.cfg
+    log(f"[gpu] gather path {name}")
+    a = run_layer(I)
+    b = run_layer(I, gather=True)
+    assert np.array_equal(a["y_perm"], b["y_perm"])
+    assert np.array_equal(a["y"], b["y"])
+    o = oracle_layer(I)
+    assert rel_max_err(f64(b["y"]), o["y"]) <= (F32_TOL if c.dtype == "f32" else BF16_TOL)
 
 
 @pytest.mark.parametrize("name", ["mixtral_small", "deepseek_small"])
