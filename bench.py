@@ -104,6 +104,68 @@ def copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes": nbytes, "ms": ms, "GBps_read_plus_write": 2 * nbytes / ms / 1e6}))
 
 
+def stream_copy_gbps(nbytes: int = 1 << 30, reps: int = 5) -> float:
+    """Practical HBM rate on this GPU: read + write bytes of a plain device copy of
+    nbytes (torch's copy kernel), median of reps, run outside any timed region."""
+    import torch
+    src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    rates = []
+    for _ in range(reps):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        dst.copy_(src)
+        ev1.record()
+        torch.cuda.synchronize()
+        rates.append(2 * nbytes / ev0.elapsed_time(ev1) / 1e6)
+    del src, dst
+    return float(np.median(rates))
+
+
+def route_probe(reps: int = 10):
+    """Bandwidth of moe_route alone at T = 2^20 tokens (E = 64: 268 MB of fp32
+    logits, more than the 256 MB Infinity Cache), cold (a 1 GiB scratch buffer is
+    written before each rep, flushing L2 and the Infinity Cache) and warm (back to
+    back).  One JSON line per (E, k)."""
+    import torch
+
+    import paper_2606_21712_amd as moe
+    T = 1 << 20
+    copy_gbs = stream_copy_gbps()
+    scratch = torch.empty(1 << 29, dtype=torch.float16, device="cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    for E, k in ((64, 4), (64, 8), (8, 2)):
+        logits = torch.randn((T, E), generator=gen, device="cuda", dtype=torch.float32)
+        ids = torch.empty((T, k), dtype=torch.int32, device="cuda")
+        w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+        for _ in range(3):
+            moe.moe_route(logits, k, topk_ids=ids, topk_weights=w)
+        torch.cuda.synchronize()
+        res = {}
+        for mode in ("cold", "warm"):
+            ts = []
+            for _ in range(reps):
+                if mode == "cold":
+                    scratch.fill_(1.0)
+                ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ev0.record()
+                moe.moe_route(logits, k, topk_ids=ids, topk_weights=w)
+                ev1.record()
+                torch.cuda.synchronize()
+                ts.append(ev0.elapsed_time(ev1) * 1e3)
+            us = float(np.median(ts))
+            gbs = (T * E * 4 + T * k * 8) / (us * 1e-6) / 1e9
+            res[mode] = dict(us=round(us, 2), GBps=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 3),
+                             frac_copy=round(gbs / copy_gbs, 3))
+        print(json.dumps({"probe": "moe_route", "tokens": T, "experts": E, "top_k": k,
+                          "bytes": T * E * 4 + T * k * 8, "stream_copy_GBps": round(copy_gbs, 1), **res}),
+              flush=True)
+        del logits, ids, w
+
+
 SWEEP_SHAPES = {
     # layer shape -> (workload whose weights and routing recipe it uses, largest T)
     "mixtral": ("mixtral4k", 65536),
@@ -184,9 +246,13 @@ def main():
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
     ap.add_argument("--sweep", choices=["mixtral", "deepseek", "memconstrained"], default=None,
                     help="expert-batch sweep of one layer shape: one JSON line per batch size")
+    ap.add_argument("--route-probe", action="store_true",
+                    help="only time moe_route at 2^20 tokens (bandwidth probe), cold and warm")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.route_probe:
+        return route_probe()
     if args.sweep:
         return expert_batch_sweep(args.sweep, args.steps, args.warmup)
 
@@ -271,12 +337,14 @@ def main():
         "combine": R * c.H * b + c.T * c.H * b * (2 if c.Fs else 1) + c.T * c.k * 8,
     }
     perm_us = sum(kernels[k]["avg_us"] for k in kernels if k.startswith("permute_"))
-    bw = {}
+    copy_gbs = stream_copy_gbps()
+    bw = {"stream_copy_GBps": round(copy_gbs, 1)}
     for name, us in (("route", kernels.get("route", {}).get("avg_us")), ("permute", perm_us),
                      ("combine", kernels.get("combine", {}).get("avg_us"))):
         if us:
             gbs = bytes_alg[name] / (us * 1e-6) / 1e9
-            bw[name] = dict(us=round(us, 2), GBps=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 3))
+            bw[name] = dict(us=round(us, 2), GBps=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 3),
+                            frac_copy=round(gbs / copy_gbs, 3))
 
     out = {
         "metric": METRIC,

@@ -3,6 +3,7 @@
 // Gather form: one wavefront per token walks the hidden dimension in 16-byte
 // vectors (8 bf16 or 4 fp32 per lane), loads the token's k expert rows, sums
 // them in fp32 in slot order, adds the shared-expert row last and rounds once.
+// For k = 1, 2, 4, 8 the loads of all k rows are in flight together.
 // Every output element is written by exactly one lane, so there are no atomics
 // and the result is deterministic.
 #include "common.h"
@@ -50,7 +51,10 @@ struct Vec<false> {                // 4 fp32 in 16 bytes
   }
 };
 
-template <bool BF16, int UNROLL>
+// KT > 0: k is KT, known at compile time, and each lane first issues the loads of
+// all KT rows for UNROLL vectors (KT * UNROLL 16-byte loads in flight), then sums
+// them in slot order.  KT = 0: any k <= kMaxTopK, one row's loads at a time.
+template <bool BF16, int KT, int UNROLL>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __restrict__ y_perm,
                                                           const int32_t* __restrict__ dest,
                                                           const float* __restrict__ w,
@@ -58,14 +62,16 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __rest
                                                           int64_t T, int k, int64_t row_bytes,
                                                           uint8_t* __restrict__ y) {
   using V = Vec<BF16>;
+  constexpr int KM = KT > 0 ? KT : kMaxTopK;
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t t = int64_t(blockIdx.x) * kWavesPerBlock + wv;
   if (t >= T) return;
-  int32_t rows[kMaxTopK];
-  float wt[kMaxTopK];
+  if (KT > 0) k = KT;
+  int32_t rows[KM];
+  float wt[KM];
 #pragma unroll
-  for (int j = 0; j < kMaxTopK; ++j) {
+  for (int j = 0; j < KM; ++j) {
     rows[j] = j < k ? dest[t * k + j] : 0;
     wt[j] = j < k ? w[t * k + j] : 0.f;
   }
@@ -76,21 +82,43 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __rest
     for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
       for (int i = 0; i < V::N; ++i) acc[u][i] = 0.f;
+    if (KT > 0) {
+      u32x4 raw[KM][UNROLL];
 #pragma unroll
-    for (int j = 0; j < kMaxTopK; ++j) {
-      if (j < k) {
+      for (int j = 0; j < KM; ++j) {
         const u32x4* src = reinterpret_cast<const u32x4*>(y_perm + int64_t(rows[j]) * row_bytes);
-        u32x4 raw[UNROLL];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
-          if (v0 + u * kWave < nvec) raw[u] = __builtin_nontemporal_load(src + v0 + u * kWave);
+          if (v0 + u * kWave < nvec) raw[j][u] = __builtin_nontemporal_load(src + v0 + u * kWave);
+      }
+#pragma unroll
+      for (int j = 0; j < KM; ++j)
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
           if (v0 + u * kWave < nvec) {
             float f[V::N];
-            V::unpack(raw[u], f);
+            V::unpack(raw[j][u], f);
 #pragma unroll
             for (int i = 0; i < V::N; ++i) acc[u][i] = fmaf(wt[j], f[i], acc[u][i]);
+          }
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        if (j < k) {
+          const u32x4* src = reinterpret_cast<const u32x4*>(y_perm + int64_t(rows[j]) * row_bytes);
+          u32x4 raw[UNROLL];
+#pragma unroll
+          for (int u = 0; u < UNROLL; ++u)
+            if (v0 + u * kWave < nvec) raw[u] = __builtin_nontemporal_load(src + v0 + u * kWave);
+#pragma unroll
+          for (int u = 0; u < UNROLL; ++u) {
+            if (v0 + u * kWave < nvec) {
+              float f[V::N];
+              V::unpack(raw[u], f);
+#pragma unroll
+              for (int i = 0; i < V::N; ++i) acc[u][i] = fmaf(wt[j], f[i], acc[u][i]);
+            }
           }
         }
       }
@@ -114,6 +142,32 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __rest
   }
 }
 
+template <bool BF16>
+void launch_combine_t(const uint8_t* yp, const int32_t* dest, const float* w, const uint8_t* ys, int64_t T,
+                      int k, int64_t row_bytes, uint8_t* yo, unsigned blocks, hipStream_t s) {
+  switch (k) {
+    case 1:
+      MOE_LAUNCH("combine", (combine_kernel<BF16, 1, 8>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
+                 k, row_bytes, yo);
+      break;
+    case 2:
+      MOE_LAUNCH("combine", (combine_kernel<BF16, 2, 8>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
+                 k, row_bytes, yo);
+      break;
+    case 4:
+      MOE_LAUNCH("combine", (combine_kernel<BF16, 4, 4>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
+                 k, row_bytes, yo);
+      break;
+    case 8:
+      MOE_LAUNCH("combine", (combine_kernel<BF16, 8, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
+                 k, row_bytes, yo);
+      break;
+    default:
+      MOE_LAUNCH("combine", (combine_kernel<BF16, 0, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
+                 k, row_bytes, yo);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
@@ -124,11 +178,9 @@ hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* 
   auto ys = static_cast<const uint8_t*>(y_shared);
   auto yo = static_cast<uint8_t*>(y);
   if (bf16)
-    MOE_LAUNCH("combine", (combine_kernel<true, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys,
-               T, k, row_bytes, yo);
+    launch_combine_t<true>(yp, dest, w, ys, T, k, row_bytes, yo, blocks, s);
   else
-    MOE_LAUNCH("combine", (combine_kernel<false, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys,
-               T, k, row_bytes, yo);
+    launch_combine_t<false>(yp, dest, w, ys, T, k, row_bytes, yo, blocks, s);
   return hipGetLastError();
 }
 

@@ -163,17 +163,24 @@ def test_permute_large_ids_direct():
 
 
 def test_combine_direct():
-    """Combine alone on random y_perm / weights / shared rows.  Per element,
-    |gpu - oracle| <= 2^-8 * (sum_j |w_j y_j| + |y_s|): one bf16 rounding (2^-9)
-    plus fp32 summation of at most 17 terms."""
+    """Combine alone on random y_perm / weights / shared rows, bf16 and fp32.  Per
+    element, |gpu - oracle| <= 2^-8 * (sum_j |w_j y_j| + |y_s|): one bf16 rounding
+    (2^-9) plus fp32 summation of at most 17 terms (fp32 output: far inside)."""
     rng = np.random.default_rng(7)
-    for (T, k, H, shared) in [(999, 4, 192, True), (64, 16, 64, False), (1, 1, 128, True)]:
+    # k = 1, 2, 4, 8 take the kernels with every row's loads in flight, other k the
+    # generic one; H = 4160 needs two passes of the widest unroll, with a ragged tail.
+    for (T, k, H, shared, bf16) in [(999, 4, 192, True, True), (64, 16, 64, False, True),
+                                    (1, 1, 128, True, True), (77, 8, 576, True, True),
+                                    (50, 2, 4160, False, True), (33, 1, 1024, True, True),
+                                    (41, 3, 320, True, True), (90, 8, 704, True, False),
+                                    (37, 2, 4160, True, False), (20, 5, 64, False, False)]:
         R = T * k
-        yp = moegen.round_bf16(rng.standard_normal((R, H)).astype(np.float32))
+        cast = moegen.round_bf16 if bf16 else (lambda a: a)
+        yp = cast(rng.standard_normal((R, H)).astype(np.float32))
         dest = rng.permutation(R).reshape(T, k).astype(np.int32)
         w = rng.random((T, k)).astype(np.float32)
-        ys = moegen.round_bf16(rng.standard_normal((T, H)).astype(np.float32)) if shared else None
-        log(f"[gpu] combine T={T} k={k} H={H} shared={shared}")
+        ys = cast(rng.standard_normal((T, H)).astype(np.float32)) if shared else None
+        log(f"[gpu] combine T={T} k={k} H={H} shared={shared} bf16={bf16}")
         y = moe.moe_combine(to_dev(yp), to_dev(dest), to_dev(w), None if ys is None else to_dev(ys))
         torch.cuda.synchronize()
         ref = oracle.combine(yp, dest, w, ys)
