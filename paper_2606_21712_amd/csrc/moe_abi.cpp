@@ -72,8 +72,11 @@ moe_status moe_route(const float* logits, int64_t T, int32_t E, int32_t k, int32
                      int32_t* topk_ids, float* topk_weights, moe_stream stream) {
   moe::Check c = moe::validate_route(logits, T, E, k, renormalize, topk_ids, topk_weights);
   if (!c.ok() || T == 0) return finish(c);
+  hipError_t err;
+  const int ncu = cu_count(&err);
+  if (err != hipSuccess) return hip_status("moe_route", err);
   return hip_status("moe_route",
-                    moe::launch_route(logits, T, E, k, renormalize, topk_ids, topk_weights,
+                    moe::launch_route(logits, T, E, k, renormalize, topk_ids, topk_weights, ncu,
                                       stream_of(stream)));
 }
 

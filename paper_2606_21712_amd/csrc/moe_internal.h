@@ -23,7 +23,7 @@ constexpr int kMaxExperts = 256;
 
 void route_shape(int E, int* G, int* V);
 hipError_t launch_route(const float* logits, int64_t T, int E, int k, int renorm, int32_t* ids,
-                        float* w, hipStream_t s);
+                        float* w, int num_cu, hipStream_t s);
 
 hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, int k, int H, int elt,
                           int32_t* counts, int32_t* offsets, int32_t* sorted_tok, int32_t* dest,

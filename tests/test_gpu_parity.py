@@ -132,7 +132,9 @@ def test_route_without_renormalize(name):
 def test_route_ties_and_signed_zero():
     """Integer-valued logits force ties (lower id wins); -0.0 equals +0.0."""
     rng = np.random.default_rng(5)
-    for (T, E, k) in [(1000, 8, 2), (513, 64, 8), (77, 256, 16), (64, 3, 3), (200, 100, 7)]:
+    # segment widths 1, 2, 4, 8, 16, 32 lanes per token; odd and even values per lane
+    for (T, E, k) in [(1000, 8, 2), (513, 64, 8), (77, 256, 16), (64, 3, 3), (200, 100, 7),
+                      (300, 16, 4), (300, 32, 5), (150, 129, 9), (90, 40, 6)]:
         logits = rng.integers(-2, 3, size=(T, E)).astype(np.float32)
         logits[::7, 0] = -0.0
         logits[::5, 1] = 0.0
