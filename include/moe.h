@@ -169,6 +169,71 @@ moe_status moe_grouped_ffn_gather(const void* x, const int32_t* sorted_token_ids
                                   size_t ws_bytes, moe_stream stream);
 
 /*
+ * MXFP8 expert GEMMs (the paper's MoE GEMMs are FP8: Section 5, the prefill
+ * cost estimate with FP8 MoE GEMMs, and Section 5.6).  MXFP8 is the OCP
+ * Microscaling format: E4M3 element codes (1 sign, 4 exponent bits with bias 7,
+ * 3 mantissa bits; largest value 448) and one E8M0 scale 2^(s - 127) per 32
+ * consecutive elements along k, which gfx950's block-scaled MFMA applies itself.
+ *
+ * Layout of an MXFP8 matrix with `rows` rows and K columns (K % 128 == 0):
+ *   codes   u8 [rows, K]                 row-major E4M3 codes
+ *   scales  u8 [K / 128][rows][4]        the scale of row r for k in
+ *                                        [32 b, 32 b + 32) is the byte
+ *                                        scales[((b / 4) * rows + r) * 4 + b % 4]
+ * moe_mxfp8_scale_bytes(rows, K) = rows * K / 32.  An expert weight tensor
+ * [E, N, K] is the matrix of E * N rows.
+ */
+size_t moe_mxfp8_scale_bytes(int64_t rows, int32_t K);
+
+/*
+ * moe_quantize_mxfp8 - bf16 rows to MXFP8.
+ *
+ *   src      bf16 [rows_src, K]
+ *   row_map  i32 [rows_out] or NULL: output row r quantizes src row row_map[r]
+ *            (e.g. sorted_token_ids from moe_permute gives x_perm's order);
+ *            NULL requires rows_out <= rows_src and quantizes rows 0..rows_out-1
+ *   codes    u8 [rows_out, K]  out;  scales  u8, moe_mxfp8_scale_bytes(rows_out, K)  out
+ *
+ * Per block of 32: shared exponent floor(log2(max |v|)) - 8 clamped to
+ * [-127, 127] (-127 for an all-zero block); codes = v / 2^shared_exp rounded to
+ * the nearest E4M3 value, ties to an even mantissa, clamped to +-448, sign bit
+ * kept (-0 gives 0x80).  Inputs are finite (not checked).
+ * Errors: INVALID_ARGUMENT for rows_out < 0, rows_src < 0, K not a positive
+ * multiple of 128, rows_out > rows_src without a row_map, null or misaligned
+ * pointers.  Row indices are not checked (precondition: 0 <= row_map[r] < rows_src).
+ */
+moe_status moe_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t rows_out, int64_t rows_src,
+                              int32_t K, uint8_t* codes, uint8_t* scales, moe_stream stream);
+
+/*
+ * moe_grouped_ffn_mxfp8 - moe_grouped_ffn with both GEMMs on MXFP8 operands.
+ *
+ *   x_codes, x_scales    MXFP8 [R, H]    grouped rows (moe_quantize_mxfp8 with row_map =
+ *                                        sorted_token_ids)
+ *   expert_offsets       i32 [E + 1]     DEVICE array, as moe_grouped_ffn
+ *   wg_*, wu_*           MXFP8 [E * F, H] W_gate, W_up quantized along H
+ *   wd_*                 MXFP8 [E * H, F] W_down quantized along F
+ *   y_perm               bf16 [R, H]     out
+ *   ws, ws_bytes         device scratch of at least moe_grouped_ffn_mxfp8_workspace_bytes();
+ *                        it holds h [R, F] in MXFP8
+ *
+ * g and u accumulate in fp32 from the dequantized operands (the matrix cores
+ * apply the block scales), h = silu(g) * u in fp32 is quantized to MXFP8 along F
+ * as moe_quantize_mxfp8 does, and y_perm accumulates in fp32 and is rounded to
+ * bf16 (nearest even).
+ * Errors: INVALID_ARGUMENT for R < 0, R > INT32_MAX, E < 1, H or F not a
+ * positive multiple of 128, null or misaligned pointers; UNSUPPORTED for
+ * E > 256 or when a scale array or an expert matrix reaches 2 GiB;
+ * WORKSPACE_TOO_SMALL.
+ */
+size_t moe_grouped_ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F);
+moe_status moe_grouped_ffn_mxfp8(const uint8_t* x_codes, const uint8_t* x_scales,
+                                 const int32_t* expert_offsets, int64_t R, int32_t E, int32_t H, int32_t F,
+                                 const uint8_t* wg_codes, const uint8_t* wg_scales, const uint8_t* wu_codes,
+                                 const uint8_t* wu_scales, const uint8_t* wd_codes, const uint8_t* wd_scales,
+                                 void* y_perm, void* ws, size_t ws_bytes, moe_stream stream);
+
+/*
  * moe_combine - gate-weighted sum of each token's k expert outputs (the MoE
  * module's output h_out in Algorithm 1).
  *

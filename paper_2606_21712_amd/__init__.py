@@ -19,6 +19,8 @@ __all__ = [
     "MoEError", "lib", "LIB_PATH", "HEADER_PATH", "abi_version", "exported_symbols",
     "moe_route", "moe_permute", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
+    "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
+    "moe_grouped_ffn_mxfp8", "MXFP8", "quantize_weights_mxfp8", "MoELayerMXFP8",
     "profiler_start", "profiler_stop", "profiler_records",
     "DTYPE_F32", "DTYPE_BF16",
 ]
@@ -59,6 +61,11 @@ _SIGNATURES = {
     "moe_grouped_ffn_gather": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P,
                                               ctypes.c_int, _P, _P, _SZ, _P]),
     "moe_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I32, _I32, ctypes.c_int, _P, _P]),
+    "moe_mxfp8_scale_bytes": (_SZ, [_I64, _I32]),
+    "moe_quantize_mxfp8": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _P, _P]),
+    "moe_grouped_ffn_mxfp8_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I32]),
+    "moe_grouped_ffn_mxfp8": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
+                                             _P, _P, _SZ, _P]),
     "moe_profiler_start": (ctypes.c_int, [ctypes.c_int]),
     "moe_profiler_stop": (ctypes.c_int, []),
     "moe_profiler_count": (ctypes.c_int, []),
@@ -225,6 +232,70 @@ def moe_combine(y_perm, dest_rows, topk_weights, y_shared=None, y=None, stream=N
     return y
 
 
+# --------------------------------------------------------------------------- MXFP8
+class MXFP8:
+    """An MXFP8 matrix of `rows` rows and K columns: E4M3 codes u8 [rows, K] and
+    E8M0 scales u8 in the library's k-step-major layout (include/moe.h)."""
+
+    def __init__(self, codes, scales):
+        self.codes, self.scales = codes, scales
+
+    @property
+    def shape(self):
+        return tuple(self.codes.shape)
+
+
+def moe_mxfp8_scale_bytes(rows, K) -> int:
+    return lib().moe_mxfp8_scale_bytes(rows, K)
+
+
+def moe_quantize_mxfp8(src, row_map=None, out=None, stream=None):
+    """bf16 [rows_src, K] (optionally gathered through row_map i32 [rows_out]) -> MXFP8."""
+    if src.dtype != torch.bfloat16:
+        raise TypeError("moe_quantize_mxfp8 takes bf16 rows")
+    src2 = src.reshape(-1, src.shape[-1])
+    rows_src, K = src2.shape
+    rows_out = rows_src if row_map is None else row_map.shape[0]
+    dev = src.device
+    if out is None:
+        out = MXFP8(torch.empty((rows_out, K), dtype=torch.uint8, device=dev),
+                    torch.empty(max(1, moe_mxfp8_scale_bytes(rows_out, K)), dtype=torch.uint8, device=dev))
+    _dev(src2, row_map, out.codes, out.scales)
+    _check(lib().moe_quantize_mxfp8(_ptr(src2), _ptr(row_map), rows_out, rows_src, K, _ptr(out.codes),
+                                    _ptr(out.scales), _stream(stream, dev)))
+    return out
+
+
+def quantize_weights_mxfp8(w, stream=None):
+    """Expert weights bf16 [E, N, K] -> MXFP8 of the [E * N, K] matrix (codes viewed [E, N, K])."""
+    E, N, K = w.shape
+    q = moe_quantize_mxfp8(w.reshape(E * N, K), stream=stream)
+    return MXFP8(q.codes.view(E, N, K), q.scales)
+
+
+def moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F) -> int:
+    return lib().moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)
+
+
+def moe_grouped_ffn_mxfp8(x, offsets, w_gate, w_up, w_down, y_perm=None, ws=None, stream=None):
+    """x MXFP8 [R, H] (grouped rows), w_gate/w_up MXFP8 [E, F, H], w_down MXFP8 [E, H, F]
+    -> y_perm bf16 [R, H]."""
+    R, H = x.codes.shape
+    E, F, _ = w_gate.codes.shape
+    dev = x.codes.device
+    if y_perm is None:
+        y_perm = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
+    if ws is None:
+        ws = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)), dtype=torch.uint8, device=dev)
+    _dev(x.codes, x.scales, offsets, w_gate.codes, w_gate.scales, w_up.codes, w_up.scales, w_down.codes,
+         w_down.scales, y_perm, ws)
+    _check(lib().moe_grouped_ffn_mxfp8(_ptr(x.codes), _ptr(x.scales), _ptr(offsets), R, E, H, F,
+                                       _ptr(w_gate.codes), _ptr(w_gate.scales), _ptr(w_up.codes),
+                                       _ptr(w_up.scales), _ptr(w_down.codes), _ptr(w_down.scales),
+                                       _ptr(y_perm), _ptr(ws), ws.numel(), _stream(stream, dev)))
+    return y_perm
+
+
 # --------------------------------------------------------------------------- profiler
 def profiler_start(capacity: int = 4096):
     """Bracket every following kernel launch of the library with HIP events."""
@@ -295,4 +366,38 @@ class MoELayer:
                             ws=self.ws_shared, stream=stream)
         moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, self.y_shared, y=self.y,
                     stream=stream)
+        return self.y
+
+
+class MoELayerMXFP8:
+    """The layer with MXFP8 expert GEMMs (bf16 x and y): route, permute (maps only),
+    quantization of x into grouped order, the MXFP8 grouped FFN, combine.  Weights are
+    quantized once with quantize_weights_mxfp8.  ``run`` allocates nothing and does
+    not synchronize."""
+
+    def __init__(self, T, H, E, k, F, device="cuda"):
+        self.T, self.H, self.E, self.k, self.F = T, H, E, k, F
+        dev = torch.device(device)
+        R = T * k
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.topk_ids = torch.empty((T, k), **i32)
+        self.topk_weights = torch.empty((T, k), dtype=torch.float32, device=dev)
+        self.perm = dict(counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32),
+                         sorted_token_ids=torch.empty(R, **i32), dest_rows=torch.empty((T, k), **i32),
+                         x_perm=None)
+        self.ws_perm = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), dtype=torch.uint8, device=dev)
+        self.xq = MXFP8(torch.empty((R, H), dtype=torch.uint8, device=dev),
+                        torch.empty(max(1, moe_mxfp8_scale_bytes(R, H)), dtype=torch.uint8, device=dev))
+        self.y_perm = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
+        self.ws_ffn = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)), dtype=torch.uint8,
+                                  device=dev)
+        self.y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+
+    def run(self, x, logits, wq_gate, wq_up, wq_down, renormalize=1, stream=None):
+        moe_route(logits, self.k, renormalize, self.topk_ids, self.topk_weights, stream=stream)
+        moe_permute(self.topk_ids, x, self.E, out=self.perm, ws=self.ws_perm, stream=stream)
+        moe_quantize_mxfp8(x, row_map=self.perm["sorted_token_ids"], out=self.xq, stream=stream)
+        moe_grouped_ffn_mxfp8(self.xq, self.perm["offsets"], wq_gate, wq_up, wq_down, y_perm=self.y_perm,
+                              ws=self.ws_ffn, stream=stream)
+        moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, None, y=self.y, stream=stream)
         return self.y

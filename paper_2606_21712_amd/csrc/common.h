@@ -50,6 +50,17 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
   return (uint64_t(hi) << 32) | lo;
 }
 
+// Largest e in [0, E) with pref[e] <= q, given pref[0] <= q < pref[E]
+// (the expert that owns entry q of a per-expert prefix of tile counts).
+__device__ __forceinline__ int find_expert(const int32_t* pref, int E, int64_t q) {
+  int lo = 0, hi = E;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (pref[mid] <= q) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
 // Exclusive scan of one int per thread over a 256-thread block; *total = sum.
 // Every thread of the block must call it (it synchronizes the block).
 __device__ __forceinline__ int32_t block_exclusive_scan256(int32_t v, int32_t* total) {

@@ -57,16 +57,6 @@ __global__ __launch_bounds__(256) void tile_prefix_kernel(const int32_t* __restr
   if (e == 0) prefix[E] = total;
 }
 
-// Largest e in [0, E) with pref[e] <= q, given pref[0] <= q < pref[E].
-__device__ __forceinline__ int find_expert(const int32_t* pref, int E, int64_t q) {
-  int lo = 0, hi = E;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (pref[mid] <= q) lo = mid; else hi = mid;
-  }
-  return lo;
-}
-
 // ----------------------------------------------------------------------------- bf16 MFMA GEMM
 constexpr int kBM = 256;                  // activation rows per tile
 constexpr int kBN = 256;                  // weight rows per tile (GEMM-1: 128 gate + 128 up)
@@ -482,6 +472,12 @@ int grid_for(int64_t upper_tiles, int num_cu) {
 }
 
 }  // namespace
+
+hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
+                              hipStream_t s) {
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, bm, mtile_prefix, queues);
+  return hipGetLastError();
+}
 
 hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T, const int32_t* offsets,
                            int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,

@@ -155,6 +155,46 @@ moe_status moe_grouped_ffn_gather(const void* x, const int32_t* sorted_token_ids
                  w_up, w_down, dt, y_perm, ws, stream);
 }
 
+size_t moe_mxfp8_scale_bytes(int64_t rows, int32_t K) { return moe::mxfp8_scale_bytes(rows, K); }
+
+moe_status moe_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t rows_out, int64_t rows_src,
+                              int32_t K, uint8_t* codes, uint8_t* scales, moe_stream stream) {
+  moe::Check c = moe::validate_quantize_mxfp8(src, row_map, rows_out, rows_src, K, codes, scales);
+  if (!c.ok() || rows_out == 0) return finish(c);
+  hipError_t err;
+  const int ncu = cu_count(&err);
+  if (err != hipSuccess) return hip_status("moe_quantize_mxfp8", err);
+  return hip_status("moe_quantize_mxfp8",
+                    moe::launch_quantize_mxfp8(static_cast<const uint16_t*>(src), row_map, rows_out, K, codes,
+                                               scales, ncu, stream_of(stream)));
+}
+
+size_t moe_grouped_ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F) {
+  return moe::ffn_mxfp8_workspace_bytes(R, E, H, F);
+}
+
+moe_status moe_grouped_ffn_mxfp8(const uint8_t* x_codes, const uint8_t* x_scales,
+                                 const int32_t* expert_offsets, int64_t R, int32_t E, int32_t H, int32_t F,
+                                 const uint8_t* wg_codes, const uint8_t* wg_scales, const uint8_t* wu_codes,
+                                 const uint8_t* wu_scales, const uint8_t* wd_codes, const uint8_t* wd_scales,
+                                 void* y_perm, void* ws, size_t ws_bytes, moe_stream stream) {
+  moe::Check c = moe::validate_ffn_mxfp8(x_codes, x_scales, expert_offsets, R, E, H, F, wg_codes, wg_scales,
+                                         wu_codes, wu_scales, wd_codes, wd_scales, y_perm, ws, ws_bytes);
+  if (!c.ok() || R == 0) return finish(c);
+  hipError_t err;
+  const int ncu = cu_count(&err);
+  if (err != hipSuccess) return hip_status("moe_grouped_ffn_mxfp8", err);
+  auto* base = static_cast<uint8_t*>(ws);
+  auto* prefix = reinterpret_cast<int32_t*>(base);
+  auto* queues = reinterpret_cast<int32_t*>(base + moe::ffn_queue_offset(E));
+  uint8_t* h = base + moe::ffn_h_offset(E);
+  uint8_t* hs = base + moe::ffn_mxfp8_h_scales_offset(R, E, F);
+  return hip_status("moe_grouped_ffn_mxfp8",
+                    moe::launch_ffn_mxfp8(x_codes, x_scales, expert_offsets, R, E, H, F, wg_codes, wg_scales,
+                                          wu_codes, wu_scales, wd_codes, wd_scales, static_cast<uint16_t*>(y_perm),
+                                          prefix, queues, h, hs, ncu, stream_of(stream)));
+}
+
 moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float* topk_weights,
                        const void* y_shared, int64_t T, int32_t k, int32_t H, moe_dtype dt, void* y,
                        moe_stream stream) {

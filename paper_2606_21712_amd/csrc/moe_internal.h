@@ -37,6 +37,21 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
                            int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
                            uint16_t* h, float* partial, int ksplit, int num_cu, hipStream_t s);
+// Per-expert m-tile prefix of the device-side offsets (one block); zeroes the
+// GEMMs' tile-queue counters when queues != null.
+hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
+                              hipStream_t s);
+
+// MXFP8: bf16 rows -> E4M3 codes [rows_out, K] + k-step-major E8M0 scales
+// [K / 128][rows_out][4]; output row r reads source row row_map[r] (or r).
+hipError_t launch_quantize_mxfp8(const uint16_t* src, const int32_t* row_map, int64_t rows_out, int K,
+                                 uint8_t* codes, uint8_t* scales, int num_cu, hipStream_t s);
+// Grouped SwiGLU FFN on MXFP8 operands; h (MXFP8, R x F codes + scales) is device scratch.
+hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* offsets, int64_t R, int E, int H,
+                            int F, const uint8_t* wg, const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus,
+                            const uint8_t* wd, const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix,
+                            int32_t* queues, uint8_t* h, uint8_t* hs, int num_cu, hipStream_t s);
+
 hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
                           int E, int H, int F, const float* wg, const float* wu, const float* wd,
                           float* y_perm, int32_t* mtile_prefix, float* h, hipStream_t s);

@@ -206,6 +206,90 @@ Check validate_ffn_gather(const void* x, const int32_t* sorted_tok, int64_t T, c
   return Check{};
 }
 
+namespace {
+
+Check dim128(const char* fn, const char* name, int32_t v) {
+  if (v < 128 || v % 128 != 0) {
+    Check c;
+    c.status = MOE_ERR_INVALID_ARGUMENT;
+    char buf[160];
+    std::snprintf(buf, sizeof buf, "%s: %s=%d must be a positive multiple of 128", fn, name, v);
+    c.msg = buf;
+    return c;
+  }
+  return Check{};
+}
+
+}  // namespace
+
+size_t mxfp8_scale_bytes(int64_t rows, int32_t K) {
+  if (rows <= 0 || K <= 0) return 0;
+  return size_t(rows) * size_t(K) / 32;
+}
+
+size_t ffn_mxfp8_h_scales_offset(int64_t R, int32_t E, int32_t F) {
+  return ffn_h_offset(E) + align256(size_t(R) * size_t(F));
+}
+
+size_t ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F) {
+  if (R <= 0 || E < 1 || F < 1 || H < 1) return 0;
+  return ffn_mxfp8_h_scales_offset(R, E, F) + align256(mxfp8_scale_bytes(R, F));
+}
+
+Check validate_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t rows_out, int64_t rows_src,
+                              int32_t K, const void* codes, const void* scales) {
+  const char* fn = "moe_quantize_mxfp8";
+  if (rows_out < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "rows_out=%lld is negative", rows_out);
+  if (rows_src < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "rows_src=%lld is negative", rows_src);
+  MOE_TRY(dim128(fn, "K", K));
+  if (row_map == nullptr && rows_out > rows_src)
+    return fail(MOE_ERR_INVALID_ARGUMENT, fn, "rows_out=%lld > rows_src=%lld without a row_map", rows_out,
+                rows_src);
+  if (rows_out == 0) return Check{};
+  if (rows_src == 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "rows_out=%lld rows from rows_src=0", rows_out);
+  MOE_TRY(ptr(fn, "src", src));
+  if (row_map != nullptr) MOE_TRY(ptr(fn, "row_map", row_map));
+  MOE_TRY(ptr(fn, "codes", codes));
+  MOE_TRY(ptr(fn, "scales", scales));
+  return Check{};
+}
+
+Check validate_ffn_mxfp8(const void* x, const void* xs, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
+                         int32_t F, const void* wg, const void* wgs, const void* wu, const void* wus,
+                         const void* wd, const void* wds, const void* y_perm, const void* ws, size_t ws_bytes) {
+  const char* fn = "moe_grouped_ffn_mxfp8";
+  if (E < 1) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "E=%lld must be >= 1", E);
+  if (E > MOE_MAX_EXPERTS) return fail(MOE_ERR_UNSUPPORTED, fn, "E=%lld exceeds %lld", E, MOE_MAX_EXPERTS);
+  if (R < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "R=%lld is negative", R);
+  if (R > INT32_MAX) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "R=%lld exceeds INT32_MAX", R);
+  MOE_TRY(dim128(fn, "H", H));
+  MOE_TRY(dim128(fn, "F", F));
+  // 32-bit byte offsets: one expert matrix, each weight scale array, and the
+  // row scale arrays of x and h.
+  const int64_t lim = int64_t(1) << 31;
+  if (int64_t(H) * F >= lim || int64_t(E) * H * F / 32 >= lim)
+    return fail(MOE_ERR_UNSUPPORTED, fn, "H=%lld x F=%lld experts exceed the 2 GiB addressing", H, F);
+  if (R * int64_t(H > F ? H : F) / 32 >= lim)
+    return fail(MOE_ERR_UNSUPPORTED, fn, "R=%lld rows: a row scale array reaches 2 GiB", R);
+  if (R == 0) return Check{};
+  MOE_TRY(ptr(fn, "x_codes", x));
+  MOE_TRY(ptr(fn, "x_scales", xs));
+  MOE_TRY(ptr(fn, "expert_offsets", offsets));
+  MOE_TRY(ptr(fn, "wg_codes", wg));
+  MOE_TRY(ptr(fn, "wg_scales", wgs));
+  MOE_TRY(ptr(fn, "wu_codes", wu));
+  MOE_TRY(ptr(fn, "wu_scales", wus));
+  MOE_TRY(ptr(fn, "wd_codes", wd));
+  MOE_TRY(ptr(fn, "wd_scales", wds));
+  MOE_TRY(ptr(fn, "y_perm", y_perm));
+  size_t need = ffn_mxfp8_workspace_bytes(R, E, H, F);
+  if (ws_bytes < need)
+    return fail(MOE_ERR_WORKSPACE_TOO_SMALL, fn, "workspace %lld bytes < %lld needed", (long long)ws_bytes,
+                (long long)need);
+  MOE_TRY(ptr(fn, "ws", ws));
+  return Check{};
+}
+
 Check validate_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                        int64_t T, int32_t k, int32_t H, int dt, const void* y) {
   const char* fn = "moe_combine";

@@ -40,6 +40,16 @@ Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_
 Check validate_ffn_gather(const void* x, const int32_t* sorted_tok, int64_t T, const int32_t* offsets,
                           int64_t R, int32_t E, int32_t H, int32_t F, const void* wg, const void* wu,
                           const void* wd, int dt, const void* y_perm, const void* ws, size_t ws_bytes);
+// MXFP8: scales of a [rows, K] matrix; ffn workspace [prefix | queues | h codes
+// [R, F] | h scales]
+size_t mxfp8_scale_bytes(int64_t rows, int32_t K);
+size_t ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F);
+size_t ffn_mxfp8_h_scales_offset(int64_t R, int32_t E, int32_t F);
+Check validate_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t rows_out, int64_t rows_src,
+                              int32_t K, const void* codes, const void* scales);
+Check validate_ffn_mxfp8(const void* x, const void* xs, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
+                         int32_t F, const void* wg, const void* wgs, const void* wu, const void* wus,
+                         const void* wd, const void* wds, const void* y_perm, const void* ws, size_t ws_bytes);
 Check validate_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                        int64_t T, int32_t k, int32_t H, int dt, const void* y);
 

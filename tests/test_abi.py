@@ -123,6 +123,51 @@ def test_ffn_gather_validation(L):
                       ws=None, ws_bytes=0) == 0
 
 
+def quant(L, src=P, rm=None, rows_out=64, rows_src=64, K=256, codes=P, scales=P):
+    return L.moe_quantize_mxfp8(src, rm, rows_out, rows_src, K, codes, scales, S)
+
+
+def test_quantize_mxfp8_validation(L):
+    assert quant(L, K=64) == INVALID                              # K % 128
+    assert quant(L, K=0) == INVALID
+    assert quant(L, rows_out=-1) == INVALID
+    assert quant(L, rows_src=-1) == INVALID
+    assert quant(L, rows_out=65) == INVALID                       # more rows than the source, no map
+    assert b"row_map" in L.moe_last_error()
+    assert quant(L, rows_out=65, rm=P, src=None) == INVALID       # with a map it is allowed; src checked
+    assert quant(L, rows_out=5, rows_src=0, rm=P) == INVALID
+    assert quant(L, scales=P + 4) == INVALID
+    assert quant(L, codes=None) == INVALID
+    assert quant(L, rows_out=0, src=None, codes=None, scales=None) == 0
+    assert L.moe_mxfp8_scale_bytes(64, 256) == 64 * 256 // 32
+    assert L.moe_mxfp8_scale_bytes(0, 256) == 0
+
+
+def ffn8(L, x=P, xs=P, off=P, R=100, E=8, H=128, F=256, wg=P, wgs=P, wu=P, wus=P, wd=P, wds=P, yp=P, ws=P,
+         ws_bytes=1 << 30):
+    return L.moe_grouped_ffn_mxfp8(x, xs, off, R, E, H, F, wg, wgs, wu, wus, wd, wds, yp, ws, ws_bytes, S)
+
+
+def test_ffn_mxfp8_validation(L):
+    assert ffn8(L, H=192) == INVALID                              # H % 128
+    assert ffn8(L, F=64) == INVALID
+    assert ffn8(L, E=0) == INVALID
+    assert ffn8(L, E=257) == UNSUPPORTED
+    assert ffn8(L, R=-1) == INVALID
+    assert ffn8(L, R=2**31) == INVALID
+    assert ffn8(L, H=65536, F=65536) == UNSUPPORTED               # one expert matrix of 4 GiB
+    assert ffn8(L, E=256, H=16384, F=16384) == UNSUPPORTED        # weight scales of 2 GiB
+    assert ffn8(L, R=2**30, H=128, F=1024) == UNSUPPORTED         # h scales of 32 GiB / 32
+    assert ffn8(L, wds=None) == INVALID
+    assert b"wd_scales" in L.moe_last_error()
+    assert ffn8(L, xs=P + 8) == INVALID
+    need = L.moe_grouped_ffn_mxfp8_workspace_bytes(100, 8, 128, 256)
+    assert need >= 100 * 256 + 100 * 256 // 32                   # h codes + scales
+    assert ffn8(L, ws_bytes=need - 1) == WS_SMALL
+    assert ffn8(L, R=0, x=None, xs=None, off=None, wg=None, wgs=None, wu=None, wus=None, wd=None, wds=None,
+                yp=None, ws=None, ws_bytes=0) == 0
+
+
 def test_permute_maps_only_needs_no_rows(L):
     # x_perm NULL: x may be NULL too; validation passes up to the launch.  T = 0 keeps it a no-op.
     assert permute(L, T=0, x=None, xp=None, ids=None, cnt=None, off=None, st=None, dest=None, ws=None,
