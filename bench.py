@@ -166,6 +166,75 @@ def route_probe(reps: int = 10):
         del logits, ids, w
 
 
+PEAK_FP8_TFLOPS = 5000.0        # MI355X dense fp8 MFMA
+
+
+def mxfp8_bench(config: str, steps: int, warmup: int):
+    """The layer with MXFP8 expert GEMMs on one workload: one JSON line (a separate
+    measurement; the bf16 line is the headline).  Weights are quantized once, outside
+    the timed region; inside it every step routes, permutes, quantizes x, runs both
+    MXFP8 GEMMs and combines."""
+    import torch
+
+    import moegen
+    import paper_2606_21712_amd as moe
+    c = moegen.CONFIGS[config]
+    log(f"mxfp8: generating {c.name}")
+    I = moegen.make_inputs(c)
+    x, logits = to_dev(I.x, torch), to_dev(I.logits, torch)
+    wq = [moe.quantize_weights_mxfp8(to_dev(w, torch)) for w in (I.w_gate, I.w_up, I.w_down)]
+    wqs = [moe.quantize_weights_mxfp8(to_dev(w, torch)) for w in (I.ws_gate, I.ws_up, I.ws_down)] if c.Fs \
+        else [None, None, None]
+    layer = moe.MoELayerMXFP8(c.T, c.H, c.E, c.k, c.F, c.Fs)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        layer.run(x, logits, *wq, *wqs, renormalize=c.renormalize, stream=stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    moe.profiler_start(steps * 16 + 16)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    moe.profiler_stop()
+    ms = ev0.elapsed_time(ev1) / steps
+    per = {}
+    for name, t in moe.profiler_records():
+        per.setdefault(name, []).append(t)
+    kernels = {}
+    for name, ts in per.items():
+        if c.Fs and name in ("ffn_tile_prefix", "ffn_gemm1_gate_up", "ffn_gemm2_down", "quantize_mxfp8"):
+            kernels[name] = 1e3 * float(np.mean(ts[0::2]))
+            kernels[name + ".shared"] = 1e3 * float(np.mean(ts[1::2]))
+        else:
+            kernels[name] = 1e3 * float(np.mean(ts))
+    g1 = kernels["ffn_gemm1_gate_up"]
+    gemm1_flops = 4.0 * c.H * c.F * c.R
+    ffn_us = sum(v for k, v in kernels.items() if k.startswith("ffn_"))
+    ffn_tflops = c.flops() / (ffn_us * 1e-6) / 1e12
+    out = {
+        "metric": "MoE layer tokens/s with MXFP8 expert GEMMs + grouped-GEMM TFLOP/s (% fp8 MFMA peak)",
+        "value": round(c.T / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "dtype": "mxfp8 (e4m3 codes, e8m0 scale per 32; fp32 accumulation; bf16 x, y)",
+        "data": "synthetic (seeded generator; random-init expert weights, quantized once)",
+        "config": {"workload": c.name, "tokens": c.T, "hidden": c.H, "experts": c.E, "top_k": c.k,
+                   "ffn_dim": c.F, "shared_ffn_dim": c.Fs},
+        "ffn_tflops": round(ffn_tflops, 1), "ffn_frac_fp8_peak": round(ffn_tflops / PEAK_FP8_TFLOPS, 4),
+        "roofline": {"kernel": "ffn_gemm1_gate_up (mxfp8)", "bound": "mfma",
+                     "achieved": round(gemm1_flops / (g1 * 1e-6) / 1e12, 1), "peak": PEAK_FP8_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gemm1_flops / (g1 * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 4),
+                     "flops_per_launch": gemm1_flops},
+        "kernels_us": {k: round(v, 2) for k, v in kernels.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 SWEEP_SHAPES = {
     # layer shape -> (workload whose weights and routing recipe it uses, largest T)
     "mixtral": ("mixtral4k", 65536),
@@ -246,6 +315,8 @@ def main():
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
     ap.add_argument("--sweep", choices=["mixtral", "deepseek", "memconstrained"], default=None,
                     help="expert-batch sweep of one layer shape: one JSON line per batch size")
+    ap.add_argument("--mxfp8", action="store_true",
+                    help="time the layer with MXFP8 expert GEMMs on --config (a separate JSON line)")
     ap.add_argument("--route-probe", action="store_true",
                     help="only time moe_route at 2^20 tokens (bandwidth probe), cold and warm")
     args = ap.parse_args()
@@ -253,6 +324,8 @@ def main():
         return copy_calibration(args.copy_calibration)
     if args.route_probe:
         return route_probe()
+    if args.mxfp8:
+        return mxfp8_bench(args.config, args.steps, args.warmup)
     if args.sweep:
         return expert_batch_sweep(args.sweep, args.steps, args.warmup)
 

@@ -371,33 +371,47 @@ class MoELayer:
 
 class MoELayerMXFP8:
     """The layer with MXFP8 expert GEMMs (bf16 x and y): route, permute (maps only),
-    quantization of x into grouped order, the MXFP8 grouped FFN, combine.  Weights are
-    quantized once with quantize_weights_mxfp8.  ``run`` allocates nothing and does
-    not synchronize."""
+    quantization of x into grouped order, the MXFP8 grouped FFN, combine; with Fs > 0
+    an always-active shared expert (also MXFP8) over x, added with weight 1.  Weights
+    are quantized once with quantize_weights_mxfp8.  ``run`` allocates nothing and
+    does not synchronize."""
 
-    def __init__(self, T, H, E, k, F, device="cuda"):
-        self.T, self.H, self.E, self.k, self.F = T, H, E, k, F
+    def __init__(self, T, H, E, k, F, Fs=0, device="cuda"):
+        self.T, self.H, self.E, self.k, self.F, self.Fs = T, H, E, k, F, Fs
         dev = torch.device(device)
         R = T * k
         i32 = dict(dtype=torch.int32, device=dev)
+        u8 = dict(dtype=torch.uint8, device=dev)
         self.topk_ids = torch.empty((T, k), **i32)
         self.topk_weights = torch.empty((T, k), dtype=torch.float32, device=dev)
         self.perm = dict(counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32),
                          sorted_token_ids=torch.empty(R, **i32), dest_rows=torch.empty((T, k), **i32),
                          x_perm=None)
-        self.ws_perm = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), dtype=torch.uint8, device=dev)
-        self.xq = MXFP8(torch.empty((R, H), dtype=torch.uint8, device=dev),
-                        torch.empty(max(1, moe_mxfp8_scale_bytes(R, H)), dtype=torch.uint8, device=dev))
+        self.ws_perm = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), **u8)
+        self.xq = MXFP8(torch.empty((R, H), **u8), torch.empty(max(1, moe_mxfp8_scale_bytes(R, H)), **u8))
         self.y_perm = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
-        self.ws_ffn = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)), dtype=torch.uint8,
-                                  device=dev)
+        self.ws_ffn = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)), **u8)
         self.y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        if Fs:
+            self.shared_offsets = torch.tensor([0, T], **i32)
+            self.xq_tokens = MXFP8(torch.empty((T, H), **u8),
+                                   torch.empty(max(1, moe_mxfp8_scale_bytes(T, H)), **u8))
+            self.y_shared = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+            self.ws_shared = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(T, 1, H, Fs)), **u8)
+        else:
+            self.y_shared = None
 
-    def run(self, x, logits, wq_gate, wq_up, wq_down, renormalize=1, stream=None):
+    def run(self, x, logits, wq_gate, wq_up, wq_down, wqs_gate=None, wqs_up=None, wqs_down=None,
+            renormalize=1, stream=None):
         moe_route(logits, self.k, renormalize, self.topk_ids, self.topk_weights, stream=stream)
         moe_permute(self.topk_ids, x, self.E, out=self.perm, ws=self.ws_perm, stream=stream)
         moe_quantize_mxfp8(x, row_map=self.perm["sorted_token_ids"], out=self.xq, stream=stream)
         moe_grouped_ffn_mxfp8(self.xq, self.perm["offsets"], wq_gate, wq_up, wq_down, y_perm=self.y_perm,
                               ws=self.ws_ffn, stream=stream)
-        moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, None, y=self.y, stream=stream)
+        if self.Fs:
+            moe_quantize_mxfp8(x, out=self.xq_tokens, stream=stream)
+            moe_grouped_ffn_mxfp8(self.xq_tokens, self.shared_offsets, wqs_gate, wqs_up, wqs_down,
+                                  y_perm=self.y_shared, ws=self.ws_shared, stream=stream)
+        moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, self.y_shared, y=self.y,
+                    stream=stream)
         return self.y

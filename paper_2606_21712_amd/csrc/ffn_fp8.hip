@@ -73,47 +73,49 @@ __device__ __forceinline__ uint32_t e4m3_code(float v) {
 }
 
 // ----------------------------------------------------------------------------- quantize rows
-// One thread per 8 consecutive elements; the 4 threads of a 32-element block are
-// one DPP quad.  Output row r quantizes source row row_map[r] (or r).
+// A block walks whole rows (grid-stride); each thread takes 8 consecutive
+// elements per pass, so the 4 threads of a 32-element block are one DPP quad
+// (K % 128 == 0 keeps quads inside a row).  Output row r quantizes source row
+// row_map[r] (or r).
 __global__ __launch_bounds__(256) void quantize_rows_kernel(const uint16_t* __restrict__ src,
                                                            const int32_t* __restrict__ row_map,
                                                            int64_t rows_out, int K,
                                                            uint8_t* __restrict__ codes,
                                                            uint8_t* __restrict__ scales) {
   const int per_row = K / 8;
-  const int64_t total = rows_out * per_row;
-  // every quad lies inside one row (per_row % 4 == 0) and one block
-  for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx - (threadIdx.x & 3) < total;
-       idx += int64_t(gridDim.x) * blockDim.x) {
-    const bool live = idx < total;
-    const int64_t r = live ? idx / per_row : 0;
-    const int c8 = live ? int(idx - r * per_row) : 0;
-    const int64_t sr = (row_map != nullptr && live) ? int64_t(row_map[r]) : r;
-    u32x4 raw = {0u, 0u, 0u, 0u};
-    if (live) raw = *reinterpret_cast<const u32x4*>(src + sr * K + int64_t(c8) * 8);
-    float v[8];
+  for (int64_t r = blockIdx.x; r < rows_out; r += gridDim.x) {
+    const int64_t sr = row_map != nullptr ? int64_t(row_map[r]) : r;
+    const u32x4* srow = reinterpret_cast<const u32x4*>(src + sr * K);
+    uint8_t* crow = codes + r * K;
+    // the next pass's 16 bytes are loaded before this pass is encoded
+    u32x4 nxt = {0u, 0u, 0u, 0u};
+    if (int(threadIdx.x) < per_row) nxt = __builtin_nontemporal_load(srow + threadIdx.x);
+    for (int c8 = threadIdx.x; c8 < per_row; c8 += blockDim.x) {
+      const u32x4 raw = nxt;
+      if (c8 + int(blockDim.x) < per_row) nxt = __builtin_nontemporal_load(srow + c8 + blockDim.x);
+      float v[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] = __uint_as_float(raw[i] << 16);
-      v[2 * i + 1] = __uint_as_float(raw[i] & 0xFFFF0000u);
-    }
-    float amax = 0.f;
+      for (int i = 0; i < 4; ++i) {
+        v[2 * i] = __uint_as_float(raw[i] << 16);
+        v[2 * i + 1] = __uint_as_float(raw[i] & 0xFFFF0000u);
+      }
+      float amax = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
-    amax = fmaxf(amax, __uint_as_float(uint32_t(__builtin_amdgcn_update_dpp(0, int(__float_as_uint(amax)), 0xB1,
-                                                                              0xF, 0xF, false))));
-    amax = fmaxf(amax, __uint_as_float(uint32_t(__builtin_amdgcn_update_dpp(0, int(__float_as_uint(amax)), 0x4E,
-                                                                              0xF, 0xF, false))));
-    if (!live) continue;
-    const int se = mx_shared_exp(amax);
-    const float inv = mx_inv_scale(se);
-    u32x2 pk = {0u, 0u};
+      for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
+      amax = fmaxf(amax, __uint_as_float(uint32_t(
+                             __builtin_amdgcn_update_dpp(0, int(__float_as_uint(amax)), 0xB1, 0xF, 0xF, false))));
+      amax = fmaxf(amax, __uint_as_float(uint32_t(
+                             __builtin_amdgcn_update_dpp(0, int(__float_as_uint(amax)), 0x4E, 0xF, 0xF, false))));
+      const int se = mx_shared_exp(amax);
+      const float inv = mx_inv_scale(se);
+      u32x2 pk = {0u, 0u};
 #pragma unroll
-    for (int i = 0; i < 8; ++i) pk[i / 4] |= e4m3_code(v[i] * inv) << (8 * (i % 4));
-    *reinterpret_cast<u32x2*>(codes + r * K + int64_t(c8) * 8) = pk;
-    if ((c8 & 3) == 0) {
-      const int b = c8 / 4;                                 // block index along K
-      scales[(int64_t(b / 4) * rows_out + r) * 4 + (b & 3)] = uint8_t(se + 127);
+      for (int i = 0; i < 8; ++i) pk[i / 4] |= e4m3_code(v[i] * inv) << (8 * (i % 4));
+      *reinterpret_cast<u32x2*>(crow + c8 * 8) = pk;
+      if ((c8 & 3) == 0) {
+        const int blk = c8 / 4;                               // block index along K
+        scales[(int64_t(blk / 4) * rows_out + r) * 4 + (blk & 3)] = uint8_t(se + 127);
+      }
     }
   }
 }
@@ -409,8 +411,7 @@ int grid_for(int64_t upper_tiles, int num_cu) {
 
 hipError_t launch_quantize_mxfp8(const uint16_t* src, const int32_t* row_map, int64_t rows_out, int K,
                                  uint8_t* codes, uint8_t* scales, int num_cu, hipStream_t s) {
-  const int64_t threads = rows_out * (K / 8);
-  const int64_t blocks = std::min<int64_t>((threads + 255) / 256, int64_t(num_cu) * 16);
+  const int64_t blocks = std::min<int64_t>(rows_out, int64_t(num_cu) * 16);
   MOE_LAUNCH("quantize_mxfp8", quantize_rows_kernel, dim3(unsigned(std::max<int64_t>(blocks, 1))), dim3(256), s,
              src, row_map, rows_out, K, codes, scales);
   return hipGetLastError();
