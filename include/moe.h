@@ -234,6 +234,29 @@ moe_status moe_grouped_ffn_mxfp8(const uint8_t* x_codes, const uint8_t* x_scales
                                  void* y_perm, void* ws, size_t ws_bytes, moe_stream stream);
 
 /*
+ * moe_grouped_ffn_mxfp8_gather - moe_grouped_ffn_mxfp8 reading each grouped row's
+ * codes and scales straight from the token rows: row r of group e is token
+ * sorted_token_ids[r] of x.  x is then quantized once per token (T rows, no
+ * row_map) instead of once per assignment; the result equals quantizing with
+ * row_map = sorted_token_ids and calling moe_grouped_ffn_mxfp8, bit for bit.
+ *
+ *   x_codes, x_scales  MXFP8 [T, H]   token rows (T * H < 2^31)
+ *   sorted_token_ids   i32 [R]        from moe_permute
+ *   other arguments as moe_grouped_ffn_mxfp8 (same workspace size)
+ *
+ * Errors: as moe_grouped_ffn_mxfp8, plus INVALID_ARGUMENT for T < 0, R > 0 with
+ * T = 0, a NULL or misaligned sorted_token_ids; UNSUPPORTED when the codes of x
+ * reach 2 GiB.  Token ids are not checked (precondition: 0 <= id < T).
+ */
+moe_status moe_grouped_ffn_mxfp8_gather(const uint8_t* x_codes, const uint8_t* x_scales,
+                                        const int32_t* sorted_token_ids, const int32_t* expert_offsets, int64_t T,
+                                        int64_t R, int32_t E, int32_t H, int32_t F, const uint8_t* wg_codes,
+                                        const uint8_t* wg_scales, const uint8_t* wu_codes,
+                                        const uint8_t* wu_scales, const uint8_t* wd_codes,
+                                        const uint8_t* wd_scales, void* y_perm, void* ws, size_t ws_bytes,
+                                        moe_stream stream);
+
+/*
  * moe_combine - gate-weighted sum of each token's k expert outputs (the MoE
  * module's output h_out in Algorithm 1).
  *

@@ -26,7 +26,9 @@ what the gfx950 matrix cores consume natively:
 The layer (`layer_mxfp8`) is the bf16 layer of moe_oracle with the two expert
 GEMMs on MXFP8 operands: x, W_gate and W_up quantized along H; h =
 silu(g) * u computed exactly from the dequantized operands and quantized along
-F; W_down quantized along F; routing, grouping and combine as in moe_oracle.
+F; W_down quantized along F; routing, grouping and combine as in moe_oracle;
+an always-active shared expert, when given, is the same FFN on every token
+(`dense_mxfp8`), added with weight 1.
 Every product and sum is fp64 on the dequantized values; the only roundings are
 the three quantizations.
 """
@@ -126,7 +128,17 @@ def quantize_weights(w):
     return quantize_mxfp8(w)
 
 
-def layer_mxfp8(x, logits, k, w_gate, w_up, w_down, renormalize=1):
+def dense_mxfp8(x, w_gate, w_up, w_down):
+    """One expert's MXFP8 SwiGLU FFN on every row of x (the always-active shared
+    expert): Q(h) . Q(W_down)^T with h = silu(Q(x) . Q(W_gate)^T) * (Q(x) . Q(W_up)^T)."""
+    xd = roundtrip(x)
+    g = xd @ roundtrip(w_gate).T
+    u = xd @ roundtrip(w_up).T
+    h = _bf._silu(g) * u
+    return roundtrip(h) @ roundtrip(w_down).T, h
+
+
+def layer_mxfp8(x, logits, k, w_gate, w_up, w_down, renormalize=1, ws_gate=None, ws_up=None, ws_down=None):
     """The MoE layer with MXFP8 expert GEMMs; returns every intermediate.
 
     x [T, H] and the expert weights are bf16 bit patterns (or floats).  Route,
@@ -159,7 +171,11 @@ def layer_mxfp8(x, logits, k, w_gate, w_up, w_down, renormalize=1):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
         if hi > lo:
             y_perm[lo:hi] = hd[lo:hi] @ dd[e].T
-    y = _bf.combine(y_perm, dest, w)
+    y_shared = h_shared = None
+    if ws_gate is not None:
+        y_shared, h_shared = dense_mxfp8(x, ws_gate[0], ws_up[0], ws_down[0])
+    y = _bf.combine(y_perm, dest, w, y_shared)
     return dict(ids=ids, w=w, counts=counts, offsets=offsets, dest_rows=dest,
                 sorted_token_ids=sorted_tok, x_codes=xq_codes, x_scales=xq_scales,
-                h=h, h_codes=h_codes, h_scales=h_scales, y_perm=y_perm, y=y)
+                h=h, h_codes=h_codes, h_scales=h_scales, y_perm=y_perm, y_shared=y_shared,
+                h_shared=h_shared, y=y)

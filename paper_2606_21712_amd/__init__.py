@@ -20,7 +20,8 @@ __all__ = [
     "moe_route", "moe_permute", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
     "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
-    "moe_grouped_ffn_mxfp8", "MXFP8", "quantize_weights_mxfp8", "MoELayerMXFP8",
+    "moe_grouped_ffn_mxfp8", "moe_grouped_ffn_mxfp8_gather", "MXFP8", "quantize_weights_mxfp8",
+    "MoELayerMXFP8",
     "profiler_start", "profiler_stop", "profiler_records",
     "DTYPE_F32", "DTYPE_BF16",
 ]
@@ -66,6 +67,8 @@ _SIGNATURES = {
     "moe_grouped_ffn_mxfp8_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I32]),
     "moe_grouped_ffn_mxfp8": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
                                              _P, _P, _SZ, _P]),
+    "moe_grouped_ffn_mxfp8_gather": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P,
+                                                    _P, _P, _P, _P, _SZ, _P]),
     "moe_profiler_start": (ctypes.c_int, [ctypes.c_int]),
     "moe_profiler_stop": (ctypes.c_int, []),
     "moe_profiler_count": (ctypes.c_int, []),
@@ -296,6 +299,27 @@ def moe_grouped_ffn_mxfp8(x, offsets, w_gate, w_up, w_down, y_perm=None, ws=None
     return y_perm
 
 
+def moe_grouped_ffn_mxfp8_gather(x, sorted_token_ids, offsets, w_gate, w_up, w_down, y_perm=None, ws=None,
+                                 stream=None):
+    """x MXFP8 [T, H] token rows, row r of the groups = token sorted_token_ids[r] -> y_perm bf16 [R, H]."""
+    T, H = x.codes.shape
+    R = sorted_token_ids.shape[0]
+    E, F, _ = w_gate.codes.shape
+    dev = x.codes.device
+    if y_perm is None:
+        y_perm = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
+    if ws is None:
+        ws = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)), dtype=torch.uint8, device=dev)
+    _dev(x.codes, x.scales, sorted_token_ids, offsets, w_gate.codes, w_gate.scales, w_up.codes, w_up.scales,
+         w_down.codes, w_down.scales, y_perm, ws)
+    _check(lib().moe_grouped_ffn_mxfp8_gather(_ptr(x.codes), _ptr(x.scales), _ptr(sorted_token_ids),
+                                              _ptr(offsets), T, R, E, H, F, _ptr(w_gate.codes),
+                                              _ptr(w_gate.scales), _ptr(w_up.codes), _ptr(w_up.scales),
+                                              _ptr(w_down.codes), _ptr(w_down.scales), _ptr(y_perm), _ptr(ws),
+                                              ws.numel(), _stream(stream, dev)))
+    return y_perm
+
+
 # --------------------------------------------------------------------------- profiler
 def profiler_start(capacity: int = 4096):
     """Bracket every following kernel launch of the library with HIP events."""
@@ -370,14 +394,18 @@ class MoELayer:
 
 
 class MoELayerMXFP8:
-    """The layer with MXFP8 expert GEMMs (bf16 x and y): route, permute (maps only),
-    quantization of x into grouped order, the MXFP8 grouped FFN, combine; with Fs > 0
-    an always-active shared expert (also MXFP8) over x, added with weight 1.  Weights
-    are quantized once with quantize_weights_mxfp8.  ``run`` allocates nothing and
-    does not synchronize."""
+    """The layer with MXFP8 expert GEMMs (bf16 x and y); with Fs > 0 an always-active
+    shared expert (also MXFP8) over x, added with weight 1.  Weights are quantized once
+    with quantize_weights_mxfp8.  ``run`` allocates nothing and does not synchronize.
 
-    def __init__(self, T, H, E, k, F, Fs=0, device="cuda"):
+    gather=True (default): route, permute (maps only), quantize the T token rows once,
+    grouped FFN gathering the token codes, combine.
+    gather=False: quantize x into grouped order (R = T*k rows) and run the grouped FFN
+    on those rows -- bit for bit the same output."""
+
+    def __init__(self, T, H, E, k, F, Fs=0, device="cuda", gather=True):
         self.T, self.H, self.E, self.k, self.F, self.Fs = T, H, E, k, F, Fs
+        self.gather = gather
         dev = torch.device(device)
         R = T * k
         i32 = dict(dtype=torch.int32, device=dev)
@@ -388,14 +416,15 @@ class MoELayerMXFP8:
                          sorted_token_ids=torch.empty(R, **i32), dest_rows=torch.empty((T, k), **i32),
                          x_perm=None)
         self.ws_perm = torch.empty(max(1, moe_permute_workspace_bytes(T, E, k)), **u8)
-        self.xq = MXFP8(torch.empty((R, H), **u8), torch.empty(max(1, moe_mxfp8_scale_bytes(R, H)), **u8))
+        rows = T if gather else R
+        self.xq = MXFP8(torch.empty((rows, H), **u8), torch.empty(max(1, moe_mxfp8_scale_bytes(rows, H)), **u8))
         self.y_perm = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
         self.ws_ffn = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F)), **u8)
         self.y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
         if Fs:
             self.shared_offsets = torch.tensor([0, T], **i32)
-            self.xq_tokens = MXFP8(torch.empty((T, H), **u8),
-                                   torch.empty(max(1, moe_mxfp8_scale_bytes(T, H)), **u8))
+            self.xq_tokens = self.xq if gather else MXFP8(
+                torch.empty((T, H), **u8), torch.empty(max(1, moe_mxfp8_scale_bytes(T, H)), **u8))
             self.y_shared = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
             self.ws_shared = torch.empty(max(1, moe_grouped_ffn_mxfp8_workspace_bytes(T, 1, H, Fs)), **u8)
         else:
@@ -405,11 +434,17 @@ class MoELayerMXFP8:
             renormalize=1, stream=None):
         moe_route(logits, self.k, renormalize, self.topk_ids, self.topk_weights, stream=stream)
         moe_permute(self.topk_ids, x, self.E, out=self.perm, ws=self.ws_perm, stream=stream)
-        moe_quantize_mxfp8(x, row_map=self.perm["sorted_token_ids"], out=self.xq, stream=stream)
-        moe_grouped_ffn_mxfp8(self.xq, self.perm["offsets"], wq_gate, wq_up, wq_down, y_perm=self.y_perm,
-                              ws=self.ws_ffn, stream=stream)
+        if self.gather:
+            moe_quantize_mxfp8(x, out=self.xq, stream=stream)
+            moe_grouped_ffn_mxfp8_gather(self.xq, self.perm["sorted_token_ids"], self.perm["offsets"], wq_gate,
+                                         wq_up, wq_down, y_perm=self.y_perm, ws=self.ws_ffn, stream=stream)
+        else:
+            moe_quantize_mxfp8(x, row_map=self.perm["sorted_token_ids"], out=self.xq, stream=stream)
+            moe_grouped_ffn_mxfp8(self.xq, self.perm["offsets"], wq_gate, wq_up, wq_down, y_perm=self.y_perm,
+                                  ws=self.ws_ffn, stream=stream)
         if self.Fs:
-            moe_quantize_mxfp8(x, out=self.xq_tokens, stream=stream)
+            if not self.gather:
+                moe_quantize_mxfp8(x, out=self.xq_tokens, stream=stream)
             moe_grouped_ffn_mxfp8(self.xq_tokens, self.shared_offsets, wqs_gate, wqs_up, wqs_down,
                                   y_perm=self.y_shared, ws=self.ws_shared, stream=stream)
         moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, self.y_shared, y=self.y,

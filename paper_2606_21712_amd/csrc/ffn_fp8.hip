@@ -137,8 +137,9 @@ constexpr int kBufFlags = 0x00020000;
 
 struct GemmArgsF8 {
   int32_t* queue;
-  const uint8_t* act;             // [R, K] codes of the grouped rows
-  const uint8_t* act_scales;      // [K / 128][R][4]
+  const uint8_t* act;             // [R, K] codes of the grouped rows; with a gather, [T, K] token rows
+  const uint8_t* act_scales;      // [K / 128][R][4]; with a gather, [K / 128][T][4]
+  const int32_t* gather;          // [R] token of each grouped row (gather only)
   const uint8_t* w0;              // [E * N, K] (GEMM-1: W_gate; GEMM-2: W_down)
   const uint8_t* w0_scales;       // [K / 128][E * N][4]
   const uint8_t* w1;              // GEMM-1: W_up
@@ -149,6 +150,7 @@ struct GemmArgsF8 {
   const int32_t* offsets;
   const int32_t* mtile_prefix;
   int E, K, N, ntiles, R;
+  int T;                          // token rows of act (gather only)
 };
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
@@ -159,7 +161,9 @@ __device__ __forceinline__ int wave_nrow(int wn, int ni) {
   return wn * 64 + ni * 32;
 }
 
-template <bool SWIGLU>
+// GATHER: activation row r of the tile list is token row gather[r] of act (codes
+// and scales), so the grouped copy is never written.
+template <bool SWIGLU, bool GATHER>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF8 p) {
   __shared__ __attribute__((aligned(1024))) uint8_t st0[kStageBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st1[kStageBytes];
@@ -217,8 +221,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
     const int arows = min(kBM, row_end - row0);
     const int n0 = SWIGLU ? nt * 128 : nt * 256;
     const int wrows = SWIGLU ? min(128, N - n0) : min(256, N - n0);
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint8_t*>(p.act) + int64_t(row0) * K, 0, arows * K, kBufFlags);
+    const __amdgpu_buffer_rsrc_t ra =
+        GATHER ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.act), 0, p.T * K, kBufFlags)
+               : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.act) + int64_t(row0) * K, 0, arows * K,
+                                                   kBufFlags);
     const int64_t wfirst = (int64_t(e) * N + n0) * K;
     const __amdgpu_buffer_rsrc_t rw0 =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.w0) + wfirst, 0, wrows * K, kBufFlags);
@@ -226,8 +232,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
         const_cast<uint8_t*>(SWIGLU ? p.w1 : p.w0) + wfirst, 0, wrows * K, kBufFlags);
     // Scale arrays are read whole-array bounded; rows past the tile's group or
     // past N read other rows' (finite) scales, multiplied by zero codes.
+    const int64_t act_rows = GATHER ? p.T : p.R;
     const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint8_t*>(p.act_scales), 0, int(int64_t(KT) * p.R * 4), kBufFlags);
+        const_cast<uint8_t*>(p.act_scales), 0, int(int64_t(KT) * act_rows * 4), kBufFlags);
     const __amdgpu_buffer_rsrc_t rsw0 = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint8_t*>(p.w0_scales), 0, int(int64_t(KT) * EN * 4), kBufFlags);
     const __amdgpu_buffer_rsrc_t rsw1 = __builtin_amdgcn_make_buffer_rsrc(
@@ -238,8 +245,22 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
     for (int i = 0; i < 4; ++i) {
       const int r = (8 * i + wave) * 8 + qrow;
       const uint32_t cb = uint32_t(swz(r, qpos) * 16);
-      aoff[i] = uint32_t(r) * uint32_t(K) + cb;
+      if (GATHER) {
+        // the token's row; rows past the group end get an offset beyond num_records
+        const int grow = row0 + r;
+        aoff[i] = grow < row_end ? uint32_t(p.gather[grow]) * uint32_t(K) + cb : 0x80000000u;
+      } else {
+        aoff[i] = uint32_t(r) * uint32_t(K) + cb;
+      }
       woff[i] = uint32_t(SWIGLU ? (r & 127) : r) * uint32_t(K) + cb;
+    }
+    // gather: wave 1 loads the activation scales row by row (4 x 64 dwords): the
+    // byte offset of tile row 64 j + lane's token in step 0, or beyond the array
+    uint32_t stok[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int grow = row0 + 64 * j + lane;
+      stok[j] = (GATHER && wave == 1 && grow < row_end) ? uint32_t(p.gather[grow]) * 4u : 0x80000000u;
     }
     // scale rows: wave 0 loads the weight tile's 256 scale dwords (GEMM-1: lanes
     // 0-31 the 128 gate rows, lanes 32-63 the up rows), wave 1 the activation tile's
@@ -263,8 +284,17 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
         else
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw0, stage + kWScaleOff, 16, voff, 0, 0, 0);
       } else if (wave == 1) {
-        const uint32_t voff = uint32_t((int64_t(kt) * p.R + row0) * 4) + uint32_t(lane * 16);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff, 16, voff, 0, 0, 0);
+        if (GATHER) {
+          const uint32_t step_off = uint32_t(int64_t(kt) * p.T * 4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff + 256 * j, 4,
+                                                     stok[j] == 0x80000000u ? stok[j] : stok[j] + step_off, 0,
+                                                     0, 0);
+        } else {
+          const uint32_t voff = uint32_t((int64_t(kt) * p.R + row0) * 4) + uint32_t(lane * 16);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff, 16, voff, 0, 0, 0);
+        }
       }
     };
 
@@ -417,20 +447,25 @@ hipError_t launch_quantize_mxfp8(const uint16_t* src, const int32_t* row_map, in
   return hipGetLastError();
 }
 
-hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* offsets, int64_t R, int E, int H,
-                            int F, const uint8_t* wg, const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus,
-                            const uint8_t* wd, const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix,
-                            int32_t* queues, uint8_t* h, uint8_t* hs, int num_cu, hipStream_t s) {
+hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* gather, int64_t T,
+                            const int32_t* offsets, int64_t R, int E, int H, int F, const uint8_t* wg,
+                            const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus, const uint8_t* wd,
+                            const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint8_t* h,
+                            uint8_t* hs, int num_cu, hipStream_t s) {
   hipError_t err = launch_tile_prefix(offsets, E, kBM, mtile_prefix, queues, s);
   if (err != hipSuccess) return err;
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
-  GemmArgsF8 a1{queues, x, xs, wg, wgs, wu, wus, h, hs, nullptr, offsets, mtile_prefix, E, H, F, F / 128, int(R)};
-  MOE_LAUNCH("ffn_gemm1_gate_up", grouped_gemm_fp8_kernel<true>, dim3(grid_for(mtiles_upper * a1.ntiles, num_cu)),
-             dim3(kThreads), s, a1);
-  GemmArgsF8 a2{queues + 1, h, hs, wd, wds, nullptr, nullptr, nullptr, nullptr, y_perm, offsets, mtile_prefix,
-                E, F, H, (H + 255) / 256, int(R)};
-  MOE_LAUNCH("ffn_gemm2_down", grouped_gemm_fp8_kernel<false>, dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)),
-             dim3(kThreads), s, a2);
+  GemmArgsF8 a1{queues, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, offsets, mtile_prefix,
+                E, H, F, F / 128, int(R), int(T)};
+  const dim3 grid1(grid_for(mtiles_upper * a1.ntiles, num_cu));
+  if (gather != nullptr)
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_fp8_kernel<true, true>), grid1, dim3(kThreads), s, a1);
+  else
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_fp8_kernel<true, false>), grid1, dim3(kThreads), s, a1);
+  GemmArgsF8 a2{queues + 1, h, hs, nullptr, wd, wds, nullptr, nullptr, nullptr, nullptr, y_perm, offsets,
+                mtile_prefix, E, F, H, (H + 255) / 256, int(R), 0};
+  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_fp8_kernel<false, false>),
+             dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)), dim3(kThreads), s, a2);
   return hipGetLastError();
 }
 

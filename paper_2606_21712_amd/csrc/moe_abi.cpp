@@ -173,6 +173,29 @@ size_t moe_grouped_ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, in
   return moe::ffn_mxfp8_workspace_bytes(R, E, H, F);
 }
 
+namespace {
+
+moe_status run_ffn_mxfp8(const char* fn, const uint8_t* x_codes, const uint8_t* x_scales, const int32_t* gather,
+                         int64_t T, const int32_t* expert_offsets, int64_t R, int32_t E, int32_t H, int32_t F,
+                         const uint8_t* wg_codes, const uint8_t* wg_scales, const uint8_t* wu_codes,
+                         const uint8_t* wu_scales, const uint8_t* wd_codes, const uint8_t* wd_scales, void* y_perm,
+                         void* ws, moe_stream stream) {
+  hipError_t err;
+  const int ncu = cu_count(&err);
+  if (err != hipSuccess) return hip_status(fn, err);
+  auto* base = static_cast<uint8_t*>(ws);
+  auto* prefix = reinterpret_cast<int32_t*>(base);
+  auto* queues = reinterpret_cast<int32_t*>(base + moe::ffn_queue_offset(E));
+  uint8_t* h = base + moe::ffn_h_offset(E);
+  uint8_t* hs = base + moe::ffn_mxfp8_h_scales_offset(R, E, F);
+  return hip_status(fn, moe::launch_ffn_mxfp8(x_codes, x_scales, gather, T, expert_offsets, R, E, H, F, wg_codes,
+                                              wg_scales, wu_codes, wu_scales, wd_codes, wd_scales,
+                                              static_cast<uint16_t*>(y_perm), prefix, queues, h, hs, ncu,
+                                              stream_of(stream)));
+}
+
+}  // namespace
+
 moe_status moe_grouped_ffn_mxfp8(const uint8_t* x_codes, const uint8_t* x_scales,
                                  const int32_t* expert_offsets, int64_t R, int32_t E, int32_t H, int32_t F,
                                  const uint8_t* wg_codes, const uint8_t* wg_scales, const uint8_t* wu_codes,
@@ -181,18 +204,23 @@ moe_status moe_grouped_ffn_mxfp8(const uint8_t* x_codes, const uint8_t* x_scales
   moe::Check c = moe::validate_ffn_mxfp8(x_codes, x_scales, expert_offsets, R, E, H, F, wg_codes, wg_scales,
                                          wu_codes, wu_scales, wd_codes, wd_scales, y_perm, ws, ws_bytes);
   if (!c.ok() || R == 0) return finish(c);
-  hipError_t err;
-  const int ncu = cu_count(&err);
-  if (err != hipSuccess) return hip_status("moe_grouped_ffn_mxfp8", err);
-  auto* base = static_cast<uint8_t*>(ws);
-  auto* prefix = reinterpret_cast<int32_t*>(base);
-  auto* queues = reinterpret_cast<int32_t*>(base + moe::ffn_queue_offset(E));
-  uint8_t* h = base + moe::ffn_h_offset(E);
-  uint8_t* hs = base + moe::ffn_mxfp8_h_scales_offset(R, E, F);
-  return hip_status("moe_grouped_ffn_mxfp8",
-                    moe::launch_ffn_mxfp8(x_codes, x_scales, expert_offsets, R, E, H, F, wg_codes, wg_scales,
-                                          wu_codes, wu_scales, wd_codes, wd_scales, static_cast<uint16_t*>(y_perm),
-                                          prefix, queues, h, hs, ncu, stream_of(stream)));
+  return run_ffn_mxfp8("moe_grouped_ffn_mxfp8", x_codes, x_scales, nullptr, R, expert_offsets, R, E, H, F,
+                       wg_codes, wg_scales, wu_codes, wu_scales, wd_codes, wd_scales, y_perm, ws, stream);
+}
+
+moe_status moe_grouped_ffn_mxfp8_gather(const uint8_t* x_codes, const uint8_t* x_scales,
+                                        const int32_t* sorted_token_ids, const int32_t* expert_offsets, int64_t T,
+                                        int64_t R, int32_t E, int32_t H, int32_t F, const uint8_t* wg_codes,
+                                        const uint8_t* wg_scales, const uint8_t* wu_codes,
+                                        const uint8_t* wu_scales, const uint8_t* wd_codes,
+                                        const uint8_t* wd_scales, void* y_perm, void* ws, size_t ws_bytes,
+                                        moe_stream stream) {
+  moe::Check c = moe::validate_ffn_mxfp8_gather(x_codes, x_scales, sorted_token_ids, T, expert_offsets, R, E, H,
+                                                F, wg_codes, wg_scales, wu_codes, wu_scales, wd_codes, wd_scales,
+                                                y_perm, ws, ws_bytes);
+  if (!c.ok() || R == 0) return finish(c);
+  return run_ffn_mxfp8("moe_grouped_ffn_mxfp8_gather", x_codes, x_scales, sorted_token_ids, T, expert_offsets, R,
+                       E, H, F, wg_codes, wg_scales, wu_codes, wu_scales, wd_codes, wd_scales, y_perm, ws, stream);
 }
 
 moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float* topk_weights,

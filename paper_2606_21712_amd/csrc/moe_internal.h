@@ -46,11 +46,14 @@ hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mt
 // [K / 128][rows_out][4]; output row r reads source row row_map[r] (or r).
 hipError_t launch_quantize_mxfp8(const uint16_t* src, const int32_t* row_map, int64_t rows_out, int K,
                                  uint8_t* codes, uint8_t* scales, int num_cu, hipStream_t s);
-// Grouped SwiGLU FFN on MXFP8 operands; h (MXFP8, R x F codes + scales) is device scratch.
-hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* offsets, int64_t R, int E, int H,
-                            int F, const uint8_t* wg, const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus,
-                            const uint8_t* wd, const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix,
-                            int32_t* queues, uint8_t* h, uint8_t* hs, int num_cu, hipStream_t s);
+// Grouped SwiGLU FFN on MXFP8 operands; h (MXFP8, R x F codes + scales) is device
+// scratch.  x is the grouped rows [R, H], or with gather != null the token rows
+// [T, H] read through gather[r] (T * H < 2^31).
+hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* gather, int64_t T,
+                            const int32_t* offsets, int64_t R, int E, int H, int F, const uint8_t* wg,
+                            const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus, const uint8_t* wd,
+                            const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint8_t* h,
+                            uint8_t* hs, int num_cu, hipStream_t s);
 
 hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
                           int E, int H, int F, const float* wg, const float* wu, const float* wd,

@@ -290,6 +290,28 @@ Check validate_ffn_mxfp8(const void* x, const void* xs, const int32_t* offsets, 
   return Check{};
 }
 
+Check validate_ffn_mxfp8_gather(const void* x, const void* xs, const int32_t* sorted_tok, int64_t T,
+                                const int32_t* offsets, int64_t R, int32_t E, int32_t H, int32_t F, const void* wg,
+                                const void* wgs, const void* wu, const void* wus, const void* wd, const void* wds,
+                                const void* y_perm, const void* ws, size_t ws_bytes) {
+  const char* fn = "moe_grouped_ffn_mxfp8_gather";
+  if (T < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "T=%lld is negative", T);
+  if (R > 0 && T == 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "R=%lld rows but T=0 tokens", R);
+  Check c = validate_ffn_mxfp8(x, xs, offsets, R, E, H, F, wg, wgs, wu, wus, wd, wds, y_perm, ws, ws_bytes);
+  if (!c.ok()) {
+    // report under this entry point's name
+    const std::string other = "moe_grouped_ffn_mxfp8";
+    if (c.msg.compare(0, other.size(), other) == 0) c.msg = std::string(fn) + c.msg.substr(other.size());
+    return c;
+  }
+  if (R == 0) return Check{};
+  // token rows are addressed with 32-bit byte offsets
+  if (T * int64_t(H) >= (int64_t(1) << 31))
+    return fail(MOE_ERR_UNSUPPORTED, fn, "x codes of T=%lld rows reach 2 GiB for the gather", T);
+  MOE_TRY(ptr(fn, "sorted_token_ids", sorted_tok));
+  return Check{};
+}
+
 Check validate_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                        int64_t T, int32_t k, int32_t H, int dt, const void* y) {
   const char* fn = "moe_combine";

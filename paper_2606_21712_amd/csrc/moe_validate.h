@@ -50,6 +50,10 @@ Check validate_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t r
 Check validate_ffn_mxfp8(const void* x, const void* xs, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
                          int32_t F, const void* wg, const void* wgs, const void* wu, const void* wus,
                          const void* wd, const void* wds, const void* y_perm, const void* ws, size_t ws_bytes);
+Check validate_ffn_mxfp8_gather(const void* x, const void* xs, const int32_t* sorted_tok, int64_t T,
+                                const int32_t* offsets, int64_t R, int32_t E, int32_t H, int32_t F, const void* wg,
+                                const void* wgs, const void* wu, const void* wus, const void* wd, const void* wds,
+                                const void* y_perm, const void* ws, size_t ws_bytes);
 Check validate_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                        int64_t T, int32_t k, int32_t H, int dt, const void* y);
 

@@ -168,6 +168,25 @@ def test_ffn_mxfp8_validation(L):
                 yp=None, ws=None, ws_bytes=0) == 0
 
 
+def ffn8g(L, x=P, xs=P, st=P, off=P, T=50, R=100, E=8, H=128, F=256, wg=P, wgs=P, wu=P, wus=P, wd=P, wds=P, yp=P,
+          ws=P, ws_bytes=1 << 30):
+    return L.moe_grouped_ffn_mxfp8_gather(x, xs, st, off, T, R, E, H, F, wg, wgs, wu, wus, wd, wds, yp, ws,
+                                          ws_bytes, S)
+
+
+def test_ffn_mxfp8_gather_validation(L):
+    assert ffn8g(L, st=None) == INVALID
+    assert b"sorted_token_ids" in L.moe_last_error()
+    assert ffn8g(L, T=0) == INVALID
+    assert ffn8g(L, T=-1) == INVALID
+    assert ffn8g(L, H=192) == INVALID
+    assert b"moe_grouped_ffn_mxfp8_gather" in L.moe_last_error()
+    assert ffn8g(L, T=2**24, H=128) == UNSUPPORTED                 # token codes of 2 GiB
+    assert ffn8g(L, ws_bytes=10) == WS_SMALL
+    assert ffn8g(L, R=0, T=0, x=None, xs=None, st=None, off=None, wg=None, wgs=None, wu=None, wus=None, wd=None,
+                 wds=None, yp=None, ws=None, ws_bytes=0) == 0
+
+
 def test_permute_maps_only_needs_no_rows(L):
     # x_perm NULL: x may be NULL too; validation passes up to the launch.  T = 0 keeps it a no-op.
     assert permute(L, T=0, x=None, xp=None, ids=None, cnt=None, off=None, st=None, dest=None, ws=None,

@@ -89,7 +89,8 @@ CASES = {
     "f8_mixtral_small": moegen.MoEConfig("f8_mixtral_small", T=1500, H=384, E=8, k=2, F=384, seed=31),
     "f8_memc_small": moegen.MoEConfig("f8_memc_small", T=3000, H=256, E=32, k=4, F=256, seed=32,
                                       routing="lognormal", pinned_small=(1, 17, 31)),
-    "f8_deepseek_small": moegen.MoEConfig("f8_deepseek_small", T=512, H=512, E=64, k=8, F=128, seed=33),
+    "f8_deepseek_small": moegen.MoEConfig("f8_deepseek_small", T=512, H=512, E=64, k=8, F=128, Fs=256,
+                                          seed=33),
     "f8_uniform": moegen.MoEConfig("f8_uniform", T=300, H=128, E=8, k=3, F=256, seed=34, routing="uniform"),
 }
 
@@ -98,15 +99,6 @@ CASES = {
 # range with random scales (far coarser than fp32's 6e-8 per addition: the matrix
 # core adds the fp8 products at reduced internal precision).  The bound takes twice that.
 ACC = 2.0 ** -12
-
-
-def gpu_h(layer, E, R, F):
-    """The MXFP8 h the kernel wrote into its workspace: [prefix | queues | codes | scales]."""
-    ws = to_host(layer.ws_ffn)
-    h_off = ((E + 1) * 4 + 255) // 256 * 256 + 256
-    hs_off = h_off + (R * F + 255) // 256 * 256
-    codes = ws[h_off: h_off + R * F].reshape(R, F)
-    return codes, scales_rowmajor(ws[hs_off: hs_off + R * F // 32], R, F)
 
 
 def h_deviation_bound(xd, gd, ud, offsets):
@@ -157,55 +149,90 @@ def check_valid_quantization(codes, scales, h, dh):
     return differ.sum(), (codes != mxfp8.quantize_mxfp8(h)[0]).sum()
 
 
+def check_ffn(xd, offsets, w_gate, w_up, w_down, ws, y_perm, label):
+    """One MXFP8 grouped FFN of the kernel against the exact one: xd are the dequantized
+    input rows in grouped order, ws the call's workspace (holding the kernel's h)."""
+    E = w_gate.shape[0]
+    R, F = xd.shape[0], w_gate.shape[1]
+    h_ex, dh = h_deviation_bound(xd, mxfp8.roundtrip(w_gate), mxfp8.roundtrip(w_up), offsets)
+    ws_host = to_host(ws)
+    h_off = ((E + 1) * 4 + 255) // 256 * 256 + 256
+    hs_off = h_off + (R * F + 255) // 256 * 256
+    hc = ws_host[h_off: h_off + R * F].reshape(R, F)
+    hs = scales_rowmajor(ws_host[hs_off: hs_off + R * F // 32], R, F)
+    flips_s, flips_c = check_valid_quantization(hc, hs, h_ex, dh)
+    log(f"[gpu]   {label} h: {flips_s} block scales and {flips_c} of {hc.size} codes differ from the exact h's")
+    # y_perm against the fp64 product of the kernel's own h: the accumulation bound,
+    # then bf16 rounding of the output (8 significant bits: 2^-8 relative)
+    hd = mxfp8.dequantize_mxfp8(hc, hs)
+    dd = mxfp8.roundtrip(w_down)
+    yp = f64(to_host(y_perm))
+    for e in range(E):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi > lo:
+            yr = hd[lo:hi] @ dd[e].T
+            acc = ACC * (np.abs(hd[lo:hi]) @ np.abs(dd[e]).T)
+            bound = 2.0 ** -8 * (np.abs(yr) + acc) + acc + 1e-30
+            assert (np.abs(yp[lo:hi] - yr) <= bound).all(), (label, e, hi - lo)
+    return yp
+
+
+def run_mxfp8_layer(c, I, gather=True):
+    wq = [moe.quantize_weights_mxfp8(to_dev(w)) for w in (I.w_gate, I.w_up, I.w_down)]
+    wqs = [moe.quantize_weights_mxfp8(to_dev(w)) for w in (I.ws_gate, I.ws_up, I.ws_down)] if c.Fs \
+        else [None, None, None]
+    layer = moe.MoELayerMXFP8(c.T, c.H, c.E, c.k, c.F, c.Fs, gather=gather)
+    layer.run(to_dev(I.x), to_dev(I.logits), *wq, *wqs)
+    torch.cuda.synchronize()
+    return layer, wq
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_layer_mxfp8(name):
     """Unique results bit-exact (routing, grouping, x and weight codes); h checked as a
     valid quantization of the exact h within the accumulation bound; y_perm against the
     fp64 product of the kernel's own h with the quantized W_down (accumulation bound
-    plus bf16 rounding, per element); y against the combine of that y_perm."""
+    plus bf16 rounding, per element); y against the combine of those results."""
     c = CASES[name]
     I = moegen.make_inputs(c)
-    log(f"[gpu] mxfp8 layer {name} T={c.T} H={c.H} E={c.E} k={c.k} F={c.F}")
-    wq = [moe.quantize_weights_mxfp8(to_dev(w)) for w in (I.w_gate, I.w_up, I.w_down)]
-    layer = moe.MoELayerMXFP8(c.T, c.H, c.E, c.k, c.F)
-    layer.run(to_dev(I.x), to_dev(I.logits), *wq)
-    torch.cuda.synchronize()
-    ref = mxfp8.layer_mxfp8(I.x, I.logits, c.k, I.w_gate, I.w_up, I.w_down)
+    log(f"[gpu] mxfp8 layer {name} T={c.T} H={c.H} E={c.E} k={c.k} F={c.F} Fs={c.Fs}")
+    layer, wq = run_mxfp8_layer(c, I)
+    sh = (I.ws_gate, I.ws_up, I.ws_down) if c.Fs else (None, None, None)
+    ref = mxfp8.layer_mxfp8(I.x, I.logits, c.k, I.w_gate, I.w_up, I.w_down, 1, *sh)
     assert np.array_equal(to_host(layer.topk_ids), ref["ids"])
     assert np.array_equal(to_host(layer.perm["offsets"]), ref["offsets"])
     assert np.array_equal(to_host(layer.perm["dest_rows"]), ref["dest_rows"])
     st = ref["sorted_token_ids"]
-    R = st.size
-    assert np.array_equal(to_host(layer.xq.codes), ref["x_codes"][st])
-    assert np.array_equal(scales_rowmajor(to_host(layer.xq.scales), R, c.H), ref["x_scales"][st])
+    # the token rows are quantized once, in token order
+    assert np.array_equal(to_host(layer.xq.codes), ref["x_codes"])
+    assert np.array_equal(scales_rowmajor(to_host(layer.xq.scales), c.T, c.H), ref["x_scales"])
     for wt, w in zip(wq, (I.w_gate, I.w_up, I.w_down)):
         wc, wsc = mxfp8.quantize_mxfp8(w)
         rows = w.shape[0] * w.shape[1]
         assert np.array_equal(to_host(wt.codes), wc)
         assert np.array_equal(scales_rowmajor(to_host(wt.scales), rows, w.shape[2]),
                               wsc.reshape(rows, w.shape[2] // 32))
-    hc, hs = gpu_h(layer, c.E, R, c.F)
-    xd = mxfp8.dequantize_mxfp8(ref["x_codes"], ref["x_scales"])[st]
-    h_ex, dh = h_deviation_bound(xd, mxfp8.roundtrip(I.w_gate), mxfp8.roundtrip(I.w_up), ref["offsets"])
-    assert np.allclose(h_ex, ref["h"], rtol=1e-12, atol=1e-300)
-    flips_s, flips_c = check_valid_quantization(hc, hs, ref["h"], dh)
-    log(f"[gpu]   h: {flips_s} block scales and {flips_c} of {hc.size} codes differ from the exact h's")
-    # y_perm against the fp64 product of the kernel's own h: the accumulation bound,
-    # then bf16 rounding of the output (8 significant bits: 2^-8 relative)
-    hd = mxfp8.dequantize_mxfp8(hc, hs)
-    dd = mxfp8.roundtrip(I.w_down)
-    yp = f64(to_host(layer.y_perm))
-    off = ref["offsets"]
-    for e in range(c.E):
-        lo, hi = int(off[e]), int(off[e + 1])
-        if hi > lo:
-            yr = hd[lo:hi] @ dd[e].T
-            acc = ACC * (np.abs(hd[lo:hi]) @ np.abs(dd[e]).T)
-            bound = 2.0 ** -8 * (np.abs(yr) + acc) + acc + 1e-30
-            assert (np.abs(yp[lo:hi] - yr) <= bound).all(), (e, hi - lo)
-    y_ref = mxfp8._bf.combine(yp, ref["dest_rows"], ref["w"])
+    xd = mxfp8.dequantize_mxfp8(ref["x_codes"], ref["x_scales"])
+    yp = check_ffn(xd[st], ref["offsets"], I.w_gate, I.w_up, I.w_down, layer.ws_ffn, layer.y_perm, "routed")
+    ys = None
+    if c.Fs:
+        ys = check_ffn(xd, np.array([0, c.T]), I.ws_gate, I.ws_up, I.ws_down, layer.ws_shared, layer.y_shared,
+                       "shared")
+    y_ref = mxfp8._bf.combine(yp, ref["dest_rows"], ref["w"], ys)
     err = rel_max_err(f64(to_host(layer.y)), y_ref)
-    log(f"[gpu]   y rel max err {err:.2e} (against the combine of the kernel's y_perm)")
+    log(f"[gpu]   y rel max err {err:.2e} (against the combine of the kernel's expert outputs)")
     assert err <= 2.0 ** -8
     # and the whole layer stays close to the oracle's own (few flips, each small)
     assert rel_max_err(f64(to_host(layer.y)), ref["y"]) <= 0.1
+
+
+def test_layer_mxfp8_gather_equals_grouped_copy():
+    """Gathering the token codes in GEMM-1 gives the same bits as quantizing x into
+    grouped order first."""
+    c = CASES["f8_memc_small"]
+    I = moegen.make_inputs(c)
+    log("[gpu] mxfp8 gather vs grouped copy")
+    a, _ = run_mxfp8_layer(c, I, gather=True)
+    b, _ = run_mxfp8_layer(c, I, gather=False)
+    assert np.array_equal(to_host(a.y_perm), to_host(b.y_perm))
+    assert np.array_equal(to_host(a.y), to_host(b.y))

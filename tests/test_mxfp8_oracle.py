@@ -212,8 +212,23 @@ def check_layer_close_to_bf16(layer_fn):
     assert 1e-4 < rel < 0.1
 
 
+def check_layer_single_expert_and_shared(layer_fn):
+    """E = 1, k = 1: every token goes to expert 0 with weight 1, so the layer is the
+    dense MXFP8 FFN; a shared expert adds its own dense MXFP8 FFN."""
+    rng = np.random.default_rng(10)
+    x, logits, _, wg, wu, wd = small_inputs(rng, E=1)
+    out = layer_fn(x, logits[:, :1], 1, wg, wu, wd)
+    dense, _ = mxfp8.dense_mxfp8(x, wg[0], wu[0], wd[0])
+    assert np.allclose(out["y"], dense, rtol=1e-12, atol=1e-12)
+    _, _, _, sg, su, sd = small_inputs(rng, E=1)
+    out2 = layer_fn(x, logits[:, :1], 1, wg, wu, wd, 1, sg, su, sd)
+    shared, _ = mxfp8.dense_mxfp8(x, sg[0], su[0], sd[0])
+    assert np.allclose(out2["y"], dense + shared, rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("check", [check_layer_exact_inputs, check_layer_identical_experts,
-                                   check_layer_scaling, check_layer_close_to_bf16])
+                                   check_layer_scaling, check_layer_close_to_bf16,
+                                   check_layer_single_expert_and_shared])
 def test_layer(check):
     check(mxfp8.layer_mxfp8)
 
