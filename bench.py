@@ -235,6 +235,46 @@ def mxfp8_bench(config: str, steps: int, warmup: int):
     print(json.dumps(out), flush=True)
 
 
+def router_probe(reps: int = 10):
+    """moe_router_topk (router GEMM fused with the gate) on the layer shapes: time,
+    bytes read (token rows + router matrix) per second, cold (L2 and Infinity Cache
+    flushed before each rep).  One JSON line per shape."""
+    import torch
+
+    import moegen
+    import paper_2606_21712_amd as moe
+    copy_gbs = stream_copy_gbps()
+    scratch = torch.empty(1 << 29, dtype=torch.float16, device="cuda")
+    for name in ("mixtral4k", "deepseek", "memconstrained"):
+        c = moegen.CONFIGS[name]
+        I = moegen.make_inputs(c, with_weights=False)
+        x = to_dev(I.x, torch)
+        w = to_dev(I.extra["w_router"], torch)
+        ids = torch.empty((c.T, c.k), dtype=torch.int32, device="cuda")
+        wt = torch.empty((c.T, c.k), dtype=torch.float32, device="cuda")
+        for _ in range(3):
+            moe.moe_router_topk(x, w, c.k, topk_ids=ids, topk_weights=wt)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            scratch.fill_(1.0)
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ev0.record()
+            moe.moe_router_topk(x, w, c.k, topk_ids=ids, topk_weights=wt)
+            ev1.record()
+            torch.cuda.synchronize()
+            ts.append(ev0.elapsed_time(ev1) * 1e3)
+        us = float(np.median(ts))
+        nbytes = c.T * c.H * 2 + c.E * c.H * 2 + c.T * c.k * 8
+        gbs = nbytes / (us * 1e-6) / 1e9
+        print(json.dumps({"probe": "moe_router_topk", "workload": name, "tokens": c.T, "hidden": c.H,
+                          "experts": c.E, "top_k": c.k, "us": round(us, 2), "bytes": nbytes,
+                          "GBps": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 3),
+                          "frac_copy": round(gbs / copy_gbs, 3), "stream_copy_GBps": round(copy_gbs, 1),
+                          "tflops": round(2.0 * c.T * c.H * c.E / (us * 1e-6) / 1e12, 2)}), flush=True)
+        del x, w, ids, wt
+
+
 SWEEP_SHAPES = {
     # layer shape -> (workload whose weights and routing recipe it uses, largest T)
     "mixtral": ("mixtral4k", 65536),
@@ -317,6 +357,8 @@ def main():
                     help="expert-batch sweep of one layer shape: one JSON line per batch size")
     ap.add_argument("--mxfp8", action="store_true",
                     help="time the layer with MXFP8 expert GEMMs on --config (a separate JSON line)")
+    ap.add_argument("--router-probe", action="store_true",
+                    help="only time moe_router_topk (router GEMM + gate) on the layer shapes")
     ap.add_argument("--route-probe", action="store_true",
                     help="only time moe_route at 2^20 tokens (bandwidth probe), cold and warm")
     args = ap.parse_args()
@@ -324,6 +366,8 @@ def main():
         return copy_calibration(args.copy_calibration)
     if args.route_probe:
         return route_probe()
+    if args.router_probe:
+        return router_probe()
     if args.mxfp8:
         return mxfp8_bench(args.config, args.steps, args.warmup)
     if args.sweep:

@@ -64,6 +64,7 @@ typedef void* moe_stream;            /* hipStream_t */
 #define MOE_ABI_VERSION 1
 #define MOE_MAX_EXPERTS 256
 #define MOE_MAX_TOPK 16
+#define MOE_MAX_ROUTER_EXPERTS 64   /* moe_router_topk */
 
 /* ABI version of the loaded library (MOE_ABI_VERSION). */
 int moe_abi_version(void);
@@ -93,6 +94,24 @@ const char* moe_last_error(void);
  */
 moe_status moe_route(const float* logits, int64_t T, int32_t E, int32_t k, int32_t renormalize,
                      int32_t* topk_ids, float* topk_weights, moe_stream stream);
+
+/*
+ * moe_router_topk - the MoE gate with its router GEMM: logits = x . w_router^T
+ * computed on the matrix cores (bf16 operands, fp32 accumulation), then the
+ * selection and gate weights of moe_route on those fp32 logits (the MoE gate
+ * whose batch Section 7 sizes).  The logits stay on chip unless `logits` is given.
+ *
+ *   x             bf16 [T, H]   hidden states
+ *   w_router      bf16 [E, H]   router matrix, one K-contiguous row per expert
+ *   logits        f32  [T, E]   optional out (NULL: not written)
+ *   topk_ids, topk_weights      as moe_route
+ *
+ * Errors: as moe_route, plus INVALID_ARGUMENT for H not a positive multiple of
+ * 64 and UNSUPPORTED for E > 64 (MOE_MAX_ROUTER_EXPERTS).
+ */
+moe_status moe_router_topk(const void* x, const void* w_router, int64_t T, int32_t E, int32_t k, int32_t H,
+                           int32_t renormalize, float* logits, int32_t* topk_ids, float* topk_weights,
+                           moe_stream stream);
 
 /*
  * moe_permute - group the T*k (token, slot) assignments by expert and gather

@@ -286,5 +286,10 @@ def make_inputs(cfg: MoEConfig | str, seed: int | None = None, with_weights: boo
     else:
         raise ValueError(f"unknown routing {cfg.routing!r}")
 
+    extra = {}
+    if dt == "bf16":
+        # the router matrix as a bf16 [E, H] tensor (K-contiguous rows, like the
+        # expert weights), for the path that computes the logits itself
+        extra["w_router"] = round_bf16(np.ascontiguousarray(w_r.T))
     return Inputs(cfg, x, logits, w_gate, w_up, w_down, *ws, chosen=chosen,
-                  target_counts=target)
+                  target_counts=target, extra=extra)

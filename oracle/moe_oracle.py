@@ -76,6 +76,18 @@ def route(logits, k: int, renormalize: int = 1):
     return ids.astype(np.int32), p_sel / denom
 
 
+def router_logits(x, w_router):
+    """The MoE gate's router GEMM: logits[t, e] = x[t] . w_router[e] in fp64 from the
+    exact input bits (x [T, H], w_router [E, H]; the step before the gate in
+    Section 7's MoE-gate batch)."""
+    return _f64(x) @ _f64(w_router).T
+
+
+def router_topk(x, w_router, k: int, renormalize: int = 1):
+    """Router GEMM followed by the gate: route(router_logits(x, w_router))."""
+    return route(router_logits(x, w_router), k, renormalize)
+
+
 # --------------------------------------------------------------------------- permute
 def permute(ids, x, E: int):
     """Group the T*k (token, slot) assignments by expert.

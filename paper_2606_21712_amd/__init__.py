@@ -17,7 +17,7 @@ import torch
 
 __all__ = [
     "MoEError", "lib", "LIB_PATH", "HEADER_PATH", "abi_version", "exported_symbols",
-    "moe_route", "moe_permute", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
+    "moe_route", "moe_router_topk", "moe_permute", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
     "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
     "moe_grouped_ffn_mxfp8", "moe_grouped_ffn_mxfp8_gather", "MXFP8", "quantize_weights_mxfp8",
@@ -53,6 +53,7 @@ _SIGNATURES = {
     "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "moe_last_error": (ctypes.c_char_p, []),
     "moe_route": (ctypes.c_int, [_P, _I64, _I32, _I32, _I32, _P, _P, _P]),
+    "moe_router_topk": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P]),
     "moe_permute_workspace_bytes": (_SZ, [_I64, _I32, _I32]),
     "moe_permute": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P,
                                    _P, _SZ, _P]),
@@ -148,6 +149,23 @@ def moe_route(logits, k, renormalize=1, topk_ids=None, topk_weights=None, stream
     _dev(logits, topk_ids, topk_weights)
     _check(lib().moe_route(_ptr(logits), T, E, k, renormalize, _ptr(topk_ids), _ptr(topk_weights),
                            _stream(stream, logits.device)))
+    return topk_ids, topk_weights
+
+
+def moe_router_topk(x, w_router, k, renormalize=1, logits=None, topk_ids=None, topk_weights=None, stream=None):
+    """x bf16 [T, H], w_router bf16 [E, H] -> (topk_ids, topk_weights); the router
+    GEMM and the gate in one kernel.  Pass logits (f32 [T, E]) to also get them."""
+    T, H = x.shape
+    E = w_router.shape[0]
+    if x.dtype != torch.bfloat16 or w_router.dtype != torch.bfloat16:
+        raise TypeError("moe_router_topk takes bf16 x and w_router")
+    if topk_ids is None:
+        topk_ids = torch.empty((T, k), dtype=torch.int32, device=x.device)
+    if topk_weights is None:
+        topk_weights = torch.empty((T, k), dtype=torch.float32, device=x.device)
+    _dev(x, w_router, logits, topk_ids, topk_weights)
+    _check(lib().moe_router_topk(_ptr(x), _ptr(w_router), T, E, k, H, renormalize, _ptr(logits), _ptr(topk_ids),
+                                 _ptr(topk_weights), _stream(stream, x.device)))
     return topk_ids, topk_weights
 
 

@@ -80,6 +80,20 @@ moe_status moe_route(const float* logits, int64_t T, int32_t E, int32_t k, int32
                                       stream_of(stream)));
 }
 
+moe_status moe_router_topk(const void* x, const void* w_router, int64_t T, int32_t E, int32_t k, int32_t H,
+                           int32_t renormalize, float* logits, int32_t* topk_ids, float* topk_weights,
+                           moe_stream stream) {
+  moe::Check c = moe::validate_router_topk(x, w_router, T, E, k, H, renormalize, logits, topk_ids, topk_weights);
+  if (!c.ok() || T == 0) return finish(c);
+  hipError_t err;
+  const int ncu = cu_count(&err);
+  if (err != hipSuccess) return hip_status("moe_router_topk", err);
+  return hip_status("moe_router_topk",
+                    moe::launch_router_topk(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_router),
+                                            T, E, k, H, renormalize, logits, topk_ids, topk_weights, ncu,
+                                            stream_of(stream)));
+}
+
 size_t moe_permute_workspace_bytes(int64_t T, int32_t E, int32_t k) {
   return moe::permute_workspace_bytes(T, E, k);
 }

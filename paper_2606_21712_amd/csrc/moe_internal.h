@@ -22,6 +22,9 @@ void prof_end(hipStream_t s);
 constexpr int kMaxExperts = 256;
 
 void route_shape(int E, int* G, int* V);
+// Router GEMM (x [T, H] . w [E, H]^T, E <= 64) fused with the gate; logits may be null.
+hipError_t launch_router_topk(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
+                              float* logits, int32_t* ids, float* wts, int num_cu, hipStream_t s);
 hipError_t launch_route(const float* logits, int64_t T, int E, int k, int renorm, int32_t* ids,
                         float* w, int num_cu, hipStream_t s);
 

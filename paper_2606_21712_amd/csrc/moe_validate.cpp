@@ -125,6 +125,25 @@ Check validate_route(const float* logits, int64_t T, int32_t E, int32_t k, int32
   return Check{};
 }
 
+Check validate_router_topk(const void* x, const void* w, int64_t T, int32_t E, int32_t k, int32_t H,
+                           int32_t renormalize, const float* logits, const int32_t* ids, const float* wts) {
+  const char* fn = "moe_router_topk";
+  MOE_TRY(experts_topk(fn, E, k));
+  if (E > MOE_MAX_ROUTER_EXPERTS)
+    return fail(MOE_ERR_UNSUPPORTED, fn, "E=%lld exceeds %lld for the fused router", E, MOE_MAX_ROUTER_EXPERTS);
+  MOE_TRY(tokens(fn, T, k));
+  MOE_TRY(dim64(fn, "H", H));
+  if (renormalize != 0 && renormalize != 1)
+    return fail(MOE_ERR_INVALID_ARGUMENT, fn, "renormalize=%lld must be 0 or 1", renormalize);
+  if (T == 0) return Check{};
+  MOE_TRY(ptr(fn, "x", x));
+  MOE_TRY(ptr(fn, "w_router", w));
+  if (logits != nullptr) MOE_TRY(ptr(fn, "logits", logits));
+  MOE_TRY(ptr(fn, "topk_ids", ids));
+  MOE_TRY(ptr(fn, "topk_weights", wts));
+  return Check{};
+}
+
 Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, int32_t k, int32_t H,
                        int dt, const int32_t* counts, const int32_t* offsets, const int32_t* sorted_tok,
                        const int32_t* dest, const void* x_perm, const void* ws, size_t ws_bytes) {

@@ -31,6 +31,8 @@ constexpr int64_t kPermuteUnit = 1024;      // assignments per counting unit (on
 
 Check validate_route(const float* logits, int64_t T, int32_t E, int32_t k, int32_t renormalize,
                      const int32_t* ids, const float* w);
+Check validate_router_topk(const void* x, const void* w, int64_t T, int32_t E, int32_t k, int32_t H,
+                           int32_t renormalize, const float* logits, const int32_t* ids, const float* wts);
 Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, int32_t k, int32_t H,
                        int dt, const int32_t* counts, const int32_t* offsets, const int32_t* sorted_tok,
                        const int32_t* dest, const void* x_perm, const void* ws, size_t ws_bytes);

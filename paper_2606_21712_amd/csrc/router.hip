@@ -1,0 +1,236 @@
+// moe_router_topk: the MoE gate's router GEMM fused with top-k selection on gfx950.
+//
+// logits[t, e] = x[t] . w_router[e] (bf16 operands, fp32 accumulation on the
+// matrix cores), then the gate of moe_route on those fp32 logits: the k largest,
+// ties to the lower expert id, softmax over the selected (or all) logits.  The
+// logits never leave the chip unless the caller asks for them.
+//
+// One wavefront takes MB blocks of 16 tokens against all experts (E <= 64: up to
+// four 16-expert blocks of v_mfma_f32_16x16x32_bf16), streaming its token rows
+// once; the router matrix (at most 64 x H bf16) stays in L2 and is read once per
+// wavefront, so larger MB (chosen when there are enough tokens to fill the GPU)
+// reads it less often.  Loads run four k-steps of 32 ahead.  The fp32 logits go
+// through LDS to the selection, where 4 lanes hold one token's logits and each
+// round takes a quad maximum of orderable keys, then a quad minimum of the expert
+// ids holding it (DPP lane permutes).
+#include "common.h"
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int kTok = 16;                  // tokens per MFMA block
+constexpr int kUnroll = 4;                // k-steps of 32 whose loads are issued together
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ uint32_t quad_max(uint32_t v) {
+  v = max(v, dpp<0xB1>(v));              // quad_perm [1, 0, 3, 2]
+  return max(v, dpp<0x4E>(v));           // quad_perm [2, 3, 0, 1]
+}
+__device__ __forceinline__ uint32_t quad_min(uint32_t v) {
+  v = min(v, dpp<0xB1>(v));
+  return min(v, dpp<0x4E>(v));
+}
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __uint_as_float(dpp<0xB1>(__float_as_uint(v)));
+  return v + __uint_as_float(dpp<0x4E>(__float_as_uint(v)));
+}
+
+// MB 16-token blocks, NB 16-expert blocks (E <= 16 NB); KMAX slots of selection state.
+template <int MB, int NB, int KMAX>
+__global__ __launch_bounds__(64) void router_kernel(const uint16_t* __restrict__ x,
+                                                   const uint16_t* __restrict__ w, int64_t T, int E,
+                                                   int k, int H, int renormalize,
+                                                   float* __restrict__ logits_out,
+                                                   int32_t* __restrict__ topk_ids,
+                                                   float* __restrict__ topk_w) {
+  constexpr int EP = 16 * NB;
+  constexpr int V = EP / 4;                 // logits per lane in the selection (4 lanes per token)
+  __shared__ float s_log[MB * kTok][EP + 1];
+
+  const int lane = threadIdx.x;
+  const int64_t t0 = int64_t(blockIdx.x) * (MB * kTok);
+  // MFMA operand lanes: row (token or expert) lane % 16, k sub-block lane / 16 (8 values)
+  const int r16 = lane & 15;
+  const int kq = lane >> 4;
+  bool xv[MB];
+  const bf16x8* xr[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    xv[mb] = t0 + mb * kTok + r16 < T;
+    xr[mb] = reinterpret_cast<const bf16x8*>(x + (xv[mb] ? t0 + mb * kTok + r16 : 0) * H + kq * 8);
+  }
+  const bf16x8* wr[NB];
+  bool wv[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    wv[nb] = nb * 16 + r16 < E;
+    wr[nb] = reinterpret_cast<const bf16x8*>(w + int64_t(wv[nb] ? nb * 16 + r16 : 0) * H + kq * 8);
+  }
+  f32x4 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16x8 zero = {};
+
+  // k-steps of 32: operand vector index k0 / 8 (each bf16x8 covers 8 of k)
+  constexpr int U = MB * NB > 8 ? 2 : kUnroll;        // keep the operands in flight in registers
+  int k0 = 0;
+  for (; k0 + 32 * U <= H; k0 += 32 * U) {
+    bf16x8 a[U][MB], b[U][NB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        a[u][mb] = xv[mb] ? __builtin_nontemporal_load(xr[mb] + (k0 + 32 * u) / 8) : zero;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) b[u][nb] = wv[nb] ? wr[nb][(k0 + 32 * u) / 8] : zero;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][mb], b[u][nb], acc[mb][nb], 0, 0, 0);
+  }
+  for (; k0 < H; k0 += 32) {
+    bf16x8 b[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) b[nb] = wv[nb] ? wr[nb][k0 / 8] : zero;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const bf16x8 a = xv[mb] ? __builtin_nontemporal_load(xr[mb] + k0 / 8) : zero;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[nb], acc[mb][nb], 0, 0, 0);
+    }
+  }
+
+  // 16 x 16 output: lane holds tokens 4 (lane / 16) + q of expert block column lane % 16
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s_log[mb * kTok + 4 * kq + q][nb * 16 + r16] = acc[mb][nb][q];
+  __syncthreads();
+
+  // ---- selection, 16 tokens per pass: token tt = lane / 4 of the pass, lane g = lane % 4
+  // holds experts g V .. g V + V - 1
+#pragma unroll 1
+  for (int pass = 0; pass < MB; ++pass) {
+    const int tt = pass * kTok + (lane >> 2);
+    const int g = lane & 3;
+    const int64_t t = t0 + tt;
+    const bool valid = t < T;
+    const int e0 = g * V;
+    float vals[V];
+    uint32_t key[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      const bool live = e0 + v < E;
+      vals[v] = live ? s_log[tt][e0 + v] : 0.f;
+      key[v] = live ? orderable(vals[v]) : 0u;           // 0 is below every real key
+    }
+    if (logits_out != nullptr && valid) {
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+        if (e0 + v < E) logits_out[t * E + e0 + v] = vals[v];
+    }
+    uint32_t selk[KMAX];
+    uint32_t sele[KMAX];
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        uint32_t m = key[0];
+#pragma unroll
+        for (int v = 1; v < V; ++v) m = max(m, key[v]);
+        m = quad_max(m);
+        uint32_t id = 0xFFFFFFFFu;
+#pragma unroll
+        for (int v = V - 1; v >= 0; --v) id = key[v] == m ? uint32_t(e0 + v) : id;
+        id = quad_min(id);
+#pragma unroll
+        for (int v = 0; v < V; ++v) key[v] = uint32_t(e0 + v) == id ? 0u : key[v];
+        selk[j] = m;
+        sele[j] = id;
+      } else {
+        selk[j] = 0u;
+        sele[j] = 0u;
+      }
+    }
+    const float lmax = from_orderable(selk[0]);
+    float p[KMAX];
+    float denom = 0.f;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        p[j] = expf(from_orderable(selk[j]) - lmax);
+        denom += p[j];                                        // slot order
+      }
+    }
+    if (!renormalize) {
+      float s = 0.f;
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+        if (e0 + v < E) s += expf(vals[v] - lmax);
+      denom = quad_sum(s);
+    }
+    if (valid && g == 0) {
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j) {
+        if (j < k) {
+          topk_ids[t * k + j] = int32_t(sele[j]);
+          topk_w[t * k + j] = p[j] / denom;
+        }
+      }
+    }
+  }
+}
+
+template <int MB, int NB>
+hipError_t launch_mn(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
+                     float* logits, int32_t* ids, float* wts, hipStream_t s) {
+  const dim3 grid(unsigned((T + MB * kTok - 1) / (MB * kTok)));
+  if (k <= 4)
+    MOE_LAUNCH("router_topk", (router_kernel<MB, NB, 4>), grid, dim3(64), s, x, w, T, E, k, H, renorm, logits,
+               ids, wts);
+  else if (k <= 8)
+    MOE_LAUNCH("router_topk", (router_kernel<MB, NB, 8>), grid, dim3(64), s, x, w, T, E, k, H, renorm, logits,
+               ids, wts);
+  else
+    MOE_LAUNCH("router_topk", (router_kernel<MB, NB, kMaxTopK>), grid, dim3(64), s, x, w, T, E, k, H, renorm,
+               logits, ids, wts);
+  return hipGetLastError();
+}
+
+// Tokens per wavefront: 64 when that still gives every compute unit 8 wavefronts,
+// else 32, else 16.
+template <int NB>
+hipError_t launch_nb(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
+                     float* logits, int32_t* ids, float* wts, int num_cu, hipStream_t s) {
+  const int64_t waves_wanted = int64_t(num_cu) * 8;
+  if (T >= waves_wanted * 64) return launch_mn<4, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
+  if (T >= waves_wanted * 32) return launch_mn<2, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
+  return launch_mn<1, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
+}
+
+}  // namespace
+
+hipError_t launch_router_topk(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
+                              float* logits, int32_t* ids, float* wts, int num_cu, hipStream_t s) {
+  switch ((E + 15) / 16) {
+    case 1: return launch_nb<1>(x, w, T, E, k, H, renorm, logits, ids, wts, num_cu, s);
+    case 2: return launch_nb<2>(x, w, T, E, k, H, renorm, logits, ids, wts, num_cu, s);
+    case 3: return launch_nb<3>(x, w, T, E, k, H, renorm, logits, ids, wts, num_cu, s);
+    default: return launch_nb<4>(x, w, T, E, k, H, renorm, logits, ids, wts, num_cu, s);
+  }
+}
+
+}  // namespace moe

@@ -187,6 +187,23 @@ def test_ffn_mxfp8_gather_validation(L):
                  wds=None, yp=None, ws=None, ws_bytes=0) == 0
 
 
+def router(L, x=P, w=P, T=100, E=8, k=2, H=128, renorm=1, logits=None, ids=P, wts=P):
+    return L.moe_router_topk(x, w, T, E, k, H, renorm, logits, ids, wts, S)
+
+
+def test_router_topk_validation(L):
+    assert router(L, E=65) == UNSUPPORTED                          # fused router holds E <= 64
+    assert router(L, E=300) == UNSUPPORTED
+    assert router(L, k=9) == INVALID
+    assert router(L, H=96) == INVALID
+    assert router(L, renorm=3) == INVALID
+    assert router(L, T=-1) == INVALID
+    assert router(L, w=None) == INVALID
+    assert b"w_router" in L.moe_last_error()
+    assert router(L, logits=P + 4) == INVALID                      # optional, but aligned when given
+    assert router(L, T=0, x=None, w=None, ids=None, wts=None) == 0
+
+
 def test_permute_maps_only_needs_no_rows(L):
     # x_perm NULL: x may be NULL too; validation passes up to the launch.  T = 0 keeps it a no-op.
     assert permute(L, T=0, x=None, xp=None, ids=None, cnt=None, off=None, st=None, dest=None, ws=None,

@@ -245,3 +245,23 @@ MUTANTS = [
 def test_pin_catches_planted_mistake(name, check):
     with pytest.raises(AssertionError):
         check(np.random.default_rng(99))
+
+
+def test_router_logits_brute_force():
+    """The router GEMM against explicit loops on a tiny shape, and router_topk against
+    routing the brute-force logits."""
+    rng = np.random.default_rng(21)
+    T, H, E, k = 7, 12, 5, 2
+    x = rng.standard_normal((T, H))
+    w = rng.standard_normal((E, H))
+    brute = np.zeros((T, E))
+    for t in range(T):
+        for e in range(E):
+            acc = 0.0
+            for h in range(H):
+                acc += x[t, h] * w[e, h]
+            brute[t, e] = acc
+    assert np.allclose(oracle.router_logits(x, w), brute, rtol=1e-14, atol=1e-14)
+    ids, wt = oracle.router_topk(x, w, k)
+    ids2, wt2 = oracle.route(brute, k)
+    assert np.array_equal(ids, ids2) and np.allclose(wt, wt2, rtol=1e-14)
