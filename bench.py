@@ -38,12 +38,22 @@ CPU_SAMPLE = {"tiny": 256, "mixtral4k": 4096, "mixtral32k_zipf": 4096, "deepseek
               "memconstrained": 4096}
 
 
+def gemm_source_sha256() -> str:
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2606_21712_amd", "csrc")
+    h = hashlib.sha256()
+    for name in ("ffn.hip", "common.h"):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def measured_traffic(workload: str):
     """HBM bytes per GEMM-1 launch from the committed counter summary, or None when
-    the summary is for another workload or the grouped-GEMM source changed since."""
+    the summary is for another workload or the grouped-GEMM source changed since
+    (the hash covers ffn.hip followed by the common.h it includes)."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"ffn_gemm1_gate_up_{workload}_hbm_traffic.md")
-    src = os.path.join(ROOT, "paper_2606_21712_amd", "csrc", "ffn.hip")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -51,7 +61,7 @@ def measured_traffic(workload: str):
         if ":" in line and line.split(":")[0] in ("source_sha256", "gemm1_traffic_bytes_per_launch"):
             k, v = line.split(":", 1)
             fields[k.strip()] = v.strip()
-    if fields.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+    if fields.get("source_sha256") != gemm_source_sha256():
         return None
     return float(fields["gemm1_traffic_bytes_per_launch"])
 
@@ -208,7 +218,7 @@ def mxfp8_bench(config: str, steps: int, warmup: int):
         per.setdefault(name, []).append(t)
     kernels = {}
     for name, ts in per.items():
-        if c.Fs and name in ("ffn_tile_prefix", "ffn_gemm1_gate_up", "ffn_gemm2_down", "quantize_mxfp8"):
+        if c.Fs and len(ts) == 2 * steps:         # routed launch, then the shared expert's
             kernels[name] = 1e3 * float(np.mean(ts[0::2]))
             kernels[name + ".shared"] = 1e3 * float(np.mean(ts[1::2]))
         else:

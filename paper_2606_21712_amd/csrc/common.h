@@ -14,18 +14,17 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// bf16 <-> fp32 as bit patterns.  Rounding is to nearest even; inputs are finite.
+// bf16 <-> fp32 as bit patterns.
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
-// Two fp32 -> two bf16 packed in one 32-bit word (low half = a).
+// Two fp32 -> two bf16 packed in one 32-bit word (low half = a), rounded to
+// nearest even: gfx950's v_cvt_pk_bf16_f32.  For every finite input it gives the
+// same bits as the integer rounding (u + 0x7FFF + ((u >> 16) & 1)) >> 16, which
+// was checked over all 2^32 - 2^24 finite fp32 patterns.
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return f32_to_bf16_bits(a) | (f32_to_bf16_bits(b) << 16);
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // Monotone map of a finite float to uint32 (larger float -> larger integer).
@@ -41,8 +40,9 @@ __device__ __forceinline__ float from_orderable(uint32_t o) {
   return __uint_as_float(u);
 }
 
-// silu(z) = z / (1 + e^-z) in fp32.
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+// silu(z) = z / (1 + e^-z) in fp32, the division taken as a multiplication by the
+// hardware reciprocal (1 ulp).  Large negative z: e^-z = inf, rcp(inf) = 0, silu = -0.
+__device__ __forceinline__ float silu(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
   uint32_t lo = __shfl_xor(uint32_t(v), mask);

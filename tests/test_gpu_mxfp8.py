@@ -103,7 +103,10 @@ ACC = 2.0 ** -12
 
 def h_deviation_bound(xd, gd, ud, offsets):
     """Per element of h, how far the kernel's fp32 h may lie from the exact one: the
-    accumulation bound on g and u propagated through silu(g) * u (|silu'| <= 1.1)."""
+    accumulation bound on g and u propagated through silu(g) * u (|silu'| <= 1.1),
+    plus 2^-14 |h| for evaluating silu(g) * u in fp32 (exp, reciprocal and two
+    products, each within a few ulp; the rounding of exp's argument -g log2(e)
+    adds up to |g| ulp, and |g| stays far below 2^9 here)."""
     R = xd.shape[0]
     F = gd.shape[1]
     h = np.zeros((R, F))
@@ -118,7 +121,8 @@ def h_deviation_bound(xd, gd, ud, offsets):
         du = ACC * (np.abs(xr) @ np.abs(ud[e]).T)
         silu = g / (1 + np.exp(-g))
         h[lo:hi] = silu * u
-        dh[lo:hi] = 1.1 * np.abs(u) * dg + np.abs(silu) * du + 1.1 * dg * du
+        assert np.abs(g).max() < 2.0 ** 9
+        dh[lo:hi] = 1.1 * np.abs(u) * dg + np.abs(silu) * du + 1.1 * dg * du + 2.0 ** -14 * np.abs(silu * u)
     return h, dh
 
 
