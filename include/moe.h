@@ -312,6 +312,22 @@ moe_status moe_profiler_stop(void);
 int moe_profiler_count(void);
 moe_status moe_profiler_record(int i, const char** name, float* ms);
 
+/*
+ * moe_set_cu_budget - compute units the library plans its persistent grids for
+ * (a scheduling knob, not part of the layer).
+ *
+ * The grouped GEMMs, route, the fused router and the MXFP8 quantizer launch one
+ * workgroup per compute unit (or a multiple of that) and share out their work
+ * among them.  With n > 0 they plan for n compute units instead of the
+ * device's count (values above the device's count are used as given), so a
+ * caller can leave compute units to concurrent streams.  n = 0 restores the
+ * device's count.  Results do not depend on it beyond fp32 rounding: how the
+ * down projection's last round of tiles is split along k depends on the grid.
+ * Process-wide; set it between calls, not while other host threads launch.
+ * Errors: INVALID_ARGUMENT for n < 0.
+ */
+moe_status moe_set_cu_budget(int32_t n);
+
 #ifdef __cplusplus
 }
 #endif

@@ -22,7 +22,7 @@ __all__ = [
     "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
     "moe_grouped_ffn_mxfp8", "moe_grouped_ffn_mxfp8_gather", "MXFP8", "quantize_weights_mxfp8",
     "MoELayerMXFP8",
-    "profiler_start", "profiler_stop", "profiler_records",
+    "profiler_start", "profiler_stop", "profiler_records", "set_cu_budget",
     "DTYPE_F32", "DTYPE_BF16",
 ]
 
@@ -71,6 +71,7 @@ _SIGNATURES = {
     "moe_grouped_ffn_mxfp8_gather": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P,
                                                     _P, _P, _P, _P, _SZ, _P]),
     "moe_profiler_start": (ctypes.c_int, [ctypes.c_int]),
+    "moe_set_cu_budget": (ctypes.c_int, [_I32]),
     "moe_profiler_stop": (ctypes.c_int, []),
     "moe_profiler_count": (ctypes.c_int, []),
     "moe_profiler_record": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
@@ -336,6 +337,12 @@ def moe_grouped_ffn_mxfp8_gather(x, sorted_token_ids, offsets, w_gate, w_up, w_d
                                               _ptr(w_down.codes), _ptr(w_down.scales), _ptr(y_perm), _ptr(ws),
                                               ws.numel(), _stream(stream, dev)))
     return y_perm
+
+
+# --------------------------------------------------------------------------- scheduling
+def set_cu_budget(n: int = 0):
+    """Plan the persistent grids for n compute units (0: the device's count)."""
+    _check(lib().moe_set_cu_budget(n))
 
 
 # --------------------------------------------------------------------------- profiler

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "tiling.h"
+
 namespace moe {
 
 constexpr int kWave = 64;       // CDNA wavefront width
@@ -59,6 +61,70 @@ __device__ __forceinline__ int find_expert(const int32_t* pref, int E, int64_t q
     if (pref[mid] <= q) lo = mid; else hi = mid;
   }
   return lo;
+}
+
+// ----------------------------------------------------------------------------- tile list
+// The grouped GEMMs walk one flattened list of output tiles: experts in order,
+// expert e owning pref[e+1] - pref[e] m-tiles of kTileRows rows times NT n-tiles.
+// Inside an expert, blocks of up to kGroupM m-tiles are swept in groups of
+// kGroupN n-tiles with the m-tile varying fastest, so the tiles in flight at
+// one time share a few weight and activation panels.
+constexpr int kGroupN = 8;
+constexpr int kGroupM = 4;
+
+struct TileCoord {
+  int e;          // expert
+  int row0;       // first grouped row of the tile
+  int row_end;    // end of the expert's rows (the tile covers [row0, min(row0 + 256, row_end)))
+  int nt;         // n-tile index
+};
+
+// Tile L of the list; pref/off are the m-tile prefix and row offsets (E + 1
+// entries, typically staged in LDS).  All lanes pass the same L.
+__device__ __forceinline__ TileCoord decode_tile(int64_t L, const int32_t* pref, const int32_t* off, int E,
+                                                 int NT) {
+  TileCoord t;
+  t.e = __builtin_amdgcn_readfirstlane(find_expert(pref, E, L / NT));
+  const int pe = __builtin_amdgcn_readfirstlane(pref[t.e]);
+  const int mt_e = __builtin_amdgcn_readfirstlane(pref[t.e + 1]) - pe;
+  const int64_t local = L - int64_t(pe) * NT;
+  const int64_t bsz = int64_t(kGroupM) * NT;
+  const int mbi = int(local / bsz);
+  const int rem = int(local - int64_t(mbi) * bsz);
+  const int bm = min(kGroupM, mt_e - mbi * kGroupM);
+  const int ng = rem / (bm * kGroupN);
+  const int rem2 = rem - ng * bm * kGroupN;
+  const int mt = mbi * kGroupM + rem2 % bm;
+  t.nt = ng * kGroupN + rem2 / bm;
+  t.row0 = __builtin_amdgcn_readfirstlane(off[t.e]) + mt * kTileRows;
+  t.row_end = __builtin_amdgcn_readfirstlane(off[t.e + 1]);
+  return t;
+}
+
+// Tail split (constants in tiling.h): of n tiles on G persistent workgroups with
+// KT k steps each, tiles [0, full) run whole and the r tiles after them are cut
+// into s pieces each (r = 0, s = 1 when nothing is split).  The work list is the
+// full tiles, then the pieces: entry full + q is piece q % s of tile
+// full + q / s, k steps [j KT / s, (j + 1) KT / s) with j = q % s, and its fp32
+// partial sums go to partial slot q.
+struct TailPlan {
+  int64_t full;
+  int r;
+  int s;
+};
+
+__device__ __forceinline__ TailPlan tail_plan(int64_t n, int G, int KT) {
+  TailPlan t{n, 0, 1};
+  if (G < 2) return t;
+  const int64_t r = n % G;
+  if (r == 0 || 2 * r > G) return t;
+  const int pieces = min(G, kMaxTailPieces);
+  const int s = int(min(int64_t(pieces) / r, int64_t(min(KT / kMinPieceSteps, kMaxTailSplit))));
+  if (s < 2) return t;
+  t.full = n - r;
+  t.r = int(r);
+  t.s = s;
+  return t;
 }
 
 // Exclusive scan of one int per thread over a 256-thread block; *total = sum.

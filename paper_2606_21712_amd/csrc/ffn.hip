@@ -65,8 +65,7 @@ constexpr int kRowBytes = kBK * 2;        // one tile row in LDS: 128 bytes = 8 
 constexpr int kOpBytes = 256 * kRowBytes; // one operand tile: 32 KB
 constexpr int kStageBytes = 2 * kOpBytes;
 constexpr int kGemmThreads = 512;        // 8 wavefronts: 2 (m) x 4 (n), two per SIMD
-constexpr int kGroupN = 8;
-constexpr int kGroupM = 4;
+static_assert(kBM == kTileRows && kBN == kTileCols, "tile shape");
 
 struct GemmArgs {
   int32_t* queue;                 // tile counter, zeroed by tile_prefix_kernel
@@ -75,10 +74,10 @@ struct GemmArgs {
   const uint16_t* w0;             // [E, N, K] (GEMM-1: W_gate; GEMM-2: W_down)
   const uint16_t* w1;             // [E, N, K] (GEMM-1: W_up)
   uint16_t* out;                  // [R, N]
-  float* partial;                 // [ksplit, R, N] fp32 when ksplit > 1 (GEMM-2 only)
+  float* partial;                 // GEMM-2: tail-split partial slots [kMaxTailPieces][256][256] fp32
   const int32_t* offsets;         // [E + 1]
   const int32_t* mtile_prefix;    // [E + 1]
-  int E, K, N, ntiles, R, ksplit;
+  int E, K, N, ntiles, R;
   int act_bytes;                  // bytes of act (gather only; < 2^31)
 };
 
@@ -135,8 +134,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const int K = p.K;
   const int N = p.N;
   const int KT = K / kBK;
-  const int ksplit = p.ksplit;
-  const int64_t total = int64_t(s_pref[p.E]) * NT * ksplit;
+  // GEMM-2 splits the tiles of its last, partly filled round along k.
+  const TailPlan plan = SWIGLU ? TailPlan{int64_t(s_pref[p.E]) * NT, 0, 1}
+                               : tail_plan(int64_t(s_pref[p.E]) * NT, int(gridDim.x), KT);
+  const int64_t total = plan.full + int64_t(plan.r) * plan.s;
   // Tiles are handed out by one queue in the global tile order: a workgroup
   // claims the next tile with one atomic, so faster workgroups take more tiles
   // and a tile's cost (full or tail m-tile, long or short K) never unbalances the
@@ -156,29 +157,20 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     const int64_t L = s_claim[it & 1];
     if (L >= total) break;                                      // uniform: every wave leaves
     if (tid == 0) s_claim[(it + 1) & 1] = atomicAdd(p.queue, 1);
-    // ---- decode the tile (wave-uniform values, moved to scalar registers).
-    // With a k split, the ksplit pieces of one output tile are adjacent entries.
-    const int64_t Lt = L / ksplit;
-    const int split = int(L - Lt * ksplit);
-    const int kt0 = split * KT / ksplit;
-    const int kt1 = (split + 1) * KT / ksplit;
-    const int e = __builtin_amdgcn_readfirstlane(find_expert(s_pref, p.E, Lt / NT));
-    const int pe = __builtin_amdgcn_readfirstlane(s_pref[e]);
-    const int mt_e = __builtin_amdgcn_readfirstlane(s_pref[e + 1]) - pe;
-    const int64_t local = Lt - int64_t(pe) * NT;
-    // Inside an expert: blocks of up to kGroupM m-tiles, each swept in groups of
-    // kGroupN n-tiles with the m-tile varying fastest, so the tiles in flight
-    // share a few weight and activation panels.
-    const int64_t bsz = int64_t(kGroupM) * NT;
-    const int mbi = int(local / bsz);
-    const int rem = int(local - int64_t(mbi) * bsz);
-    const int bm = min(kGroupM, mt_e - mbi * kGroupM);
-    const int ng = rem / (bm * kGroupN);
-    const int rem2 = rem - ng * bm * kGroupN;
-    const int mt = mbi * kGroupM + rem2 % bm;
-    const int nt = ng * kGroupN + rem2 / bm;
-    const int row0 = __builtin_amdgcn_readfirstlane(s_off[e]) + mt * kBM;
-    const int row_end = __builtin_amdgcn_readfirstlane(s_off[e + 1]);
+    // ---- decode the entry (wave-uniform values, moved to scalar registers): a
+    // whole tile, or piece j of a tail tile (k steps kt0..kt1, partial slot).
+    int64_t Lt = L;
+    int kt0 = 0, kt1 = KT, slot = -1;
+    if (L >= plan.full) {
+      const int q = int(L - plan.full);
+      const int j = q % plan.s;
+      Lt = plan.full + q / plan.s;
+      kt0 = j * KT / plan.s;
+      kt1 = (j + 1) * KT / plan.s;
+      slot = q;
+    }
+    const TileCoord tc = decode_tile(Lt, s_pref, s_off, p.E, NT);
+    const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_end = tc.row_end;
 
     // ---- buffer resources: rows past the group end (activations) or past N
     // (weights) fall outside num_records and load as zeros.
@@ -316,19 +308,20 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
               *reinterpret_cast<u32x2*>(orow + f) = pk;
             }
           }
-        } else if (ksplit > 1) {
-          // One piece of a k split: fp32 partial sums, reduced in piece order later.
-          float* prow = p.partial + (int64_t(split) * p.R + row) * N;
+        } else if (slot >= 0) {
+          // A piece of a tail tile: fp32 partial sums in its slot, tile-local
+          // [256 rows][256 columns], added in piece order by tail_reduce_kernel.
+          float* prow = p.partial + (int64_t(slot) * kBM + (row - row0)) * kBN;
 #pragma unroll
           for (int ni = 0; ni < 2; ++ni) {
 #pragma unroll
             for (int blk = 0; blk < 4; ++blk) {
-              const int n = n0 + wn * 64 + ni * 32 + blk * 8 + khalf * 4;
-              if (n < N) {
+              const int c = wn * 64 + ni * 32 + blk * 8 + khalf * 4;
+              if (n0 + c < N) {
                 f32x4 v;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) v[q] = acc[mi][ni][blk * 4 + q];
-                *reinterpret_cast<f32x4*>(prow + n) = v;
+                *reinterpret_cast<f32x4*>(prow + c) = v;
               }
             }
           }
@@ -352,18 +345,37 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   }
 }
 
-// y[i] = bf16(sum over pieces s of partial[s][i]), pieces in order; 8 outputs per thread.
-__global__ __launch_bounds__(256) void ksplit_reduce_kernel(const float* __restrict__ partial,
-                                                           int64_t count, int ksplit,
-                                                           uint16_t* __restrict__ out) {
-  const int64_t n8 = count / 8;
-  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n8;
-       i += int64_t(gridDim.x) * blockDim.x) {
+// Tail tiles of a down projection: y = bf16(sum of the tile's piece partials, in
+// piece order).  One block per tail tile (blocks past the plan's r exit); G and KT
+// are the GEMM's grid size and k steps, so the plan is the GEMM's own.
+__global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restrict__ partial,
+                                                         const int32_t* __restrict__ mtile_prefix,
+                                                         const int32_t* __restrict__ offsets, int E, int NT, int G,
+                                                         int KT, int N, uint16_t* __restrict__ y) {
+  __shared__ int32_t s_pref[kMaxExperts + 1];
+  __shared__ int32_t s_off[kMaxExperts + 1];
+  for (int i = threadIdx.x; i <= E; i += blockDim.x) {
+    s_pref[i] = mtile_prefix[i];
+    s_off[i] = offsets[i];
+  }
+  __syncthreads();
+  const TailPlan plan = tail_plan(int64_t(s_pref[E]) * NT, G, KT);
+  if (int(blockIdx.x) >= plan.r) return;                       // uniform across the block
+  const TileCoord tc = decode_tile(plan.full + blockIdx.x, s_pref, s_off, E, NT);
+  const int rows = min(kTileRows, tc.row_end - tc.row0);
+  const int n0 = tc.nt * kTileCols;
+  const int cols = min(kTileCols, N - n0);
+  const float* base = partial + int64_t(blockIdx.x) * plan.s * (kTileRows * kTileCols);
+  // 8 consecutive columns per item; a row is 32 items
+  for (int i = threadIdx.x; i < rows * (kTileCols / 8); i += blockDim.x) {
+    const int r = i / (kTileCols / 8);
+    const int c = (i % (kTileCols / 8)) * 8;
+    if (c >= cols) continue;
     float acc[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[q] = 0.f;
-    for (int s = 0; s < ksplit; ++s) {
-      const f32x4* src = reinterpret_cast<const f32x4*>(partial + s * count) + 2 * i;
+    for (int j = 0; j < plan.s; ++j) {
+      const f32x4* src = reinterpret_cast<const f32x4*>(base + (int64_t(j) * kTileRows + r) * kTileCols + c);
       const f32x4 a = __builtin_nontemporal_load(src);
       const f32x4 b = __builtin_nontemporal_load(src + 1);
 #pragma unroll
@@ -375,7 +387,7 @@ __global__ __launch_bounds__(256) void ksplit_reduce_kernel(const float* __restr
     u32x4 pk;
 #pragma unroll
     for (int q = 0; q < 4; ++q) pk[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
-    reinterpret_cast<u32x4*>(out)[i] = pk;
+    *reinterpret_cast<u32x4*>(y + int64_t(tc.row0 + r) * N + n0 + c) = pk;
   }
 }
 
@@ -473,6 +485,17 @@ int grid_for(int64_t upper_tiles, int num_cu) {
 
 }  // namespace
 
+hipError_t launch_tail_reduce(const float* partial, const int32_t* mtile_prefix, const int32_t* offsets, int E,
+                              int NT, int G, int KT, int N, uint16_t* y, hipStream_t s) {
+  // A split happens only with at least two pieces of kMinPieceSteps steps; then
+  // r <= min(G, kMaxTailPieces) / 2 tail tiles.
+  if (KT < 2 * kMinPieceSteps || G < 2) return hipSuccess;
+  const int blocks = std::min(G, kMaxTailPieces) / 2;
+  MOE_LAUNCH("ffn_tail_reduce", tail_reduce_kernel, dim3(unsigned(blocks)), dim3(256), s, partial, mtile_prefix,
+             offsets, E, NT, G, KT, N, y);
+  return hipGetLastError();
+}
+
 hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
                               hipStream_t s) {
   MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, bm, mtile_prefix, queues);
@@ -482,29 +505,26 @@ hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mt
 hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T, const int32_t* offsets,
                            int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
-                           uint16_t* h, float* partial, int ksplit, int num_cu, hipStream_t s) {
+                           uint16_t* h, float* partial, int num_cu, hipStream_t s) {
   MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix,
              queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
   GemmArgs a1{queues, act, gather, wg, wu, h, nullptr, offsets, mtile_prefix, E, H, F, (F + 127) / 128,
-              int(R), 1, int(T * H * 2)};
+              int(R), int(T * H * 2)};
   const dim3 grid1(grid_for(mtiles_upper * a1.ntiles, num_cu));
   if (gather != nullptr)
     MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, true>), grid1, dim3(kGemmThreads), s, a1);
   else
     MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, false>), grid1, dim3(kGemmThreads), s, a1);
   GemmArgs a2{queues + 1, h, nullptr, wd, nullptr, y_perm, partial, offsets, mtile_prefix, E, F, H,
-              (H + 255) / 256, int(R), ksplit, 0};
-  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_bf16_kernel<false, false>),
-             dim3(grid_for(mtiles_upper * a2.ntiles * ksplit, num_cu)), dim3(kGemmThreads), s, a2);
-  if (ksplit > 1) {
-    const int64_t count = R * H;
-    const int64_t threads = count / 8;
-    const unsigned blocks = unsigned(std::min<int64_t>((threads + 255) / 256, int64_t(num_cu) * 16));
-    MOE_LAUNCH("ffn_ksplit_reduce", ksplit_reduce_kernel, dim3(blocks), dim3(256), s, partial, count,
-               ksplit, y_perm);
-  }
+              (H + 255) / 256, int(R), 0};
+  const int grid2 = grid_for(mtiles_upper * a2.ntiles, num_cu);
+  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_bf16_kernel<false, false>), dim3(grid2), dim3(kGemmThreads), s,
+             a2);
+  const hipError_t err = launch_tail_reduce(partial, mtile_prefix, offsets, E, a2.ntiles, grid2, F / kBK, H,
+                                            y_perm, s);
+  if (err != hipSuccess) return err;
   return hipGetLastError();
 }
 

@@ -121,8 +121,7 @@ constexpr int kWScaleOff = 2 * kOpBytes;
 constexpr int kXScaleOff = 2 * kOpBytes + kScaleBytes;
 constexpr int kStageBytes = 2 * kOpBytes + 2 * kScaleBytes;
 constexpr int kThreads = 512;             // 8 wavefronts: 2 (m) x 4 (n)
-constexpr int kGroupN = 8;
-constexpr int kGroupM = 4;
+static_assert(kBM == kTileRows, "tile shape");
 constexpr int kWaitVm0 = 0x0F70;
 constexpr int kBufFlags = 0x00020000;
 
@@ -138,6 +137,7 @@ struct GemmArgsF8 {
   uint8_t* h_codes;               // GEMM-1 output [R, N]
   uint8_t* h_scales;              // [N / 128][R][4]
   uint16_t* y;                    // GEMM-2 output [R, N] bf16
+  float* partial;                 // GEMM-2: tail-split partial slots [kMaxTailPieces][256][256] fp32
   const int32_t* offsets;
   const int32_t* mtile_prefix;
   int E, K, N, ntiles, R;
@@ -181,7 +181,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
   const int N = p.N;
   const int KT = K / kBK;
   const int64_t EN = int64_t(p.E) * N;
-  const int64_t total = int64_t(s_pref[p.E]) * NT;
+  // GEMM-2 splits the tiles of its last, partly filled round along k.
+  const TailPlan plan = SWIGLU ? TailPlan{int64_t(s_pref[p.E]) * NT, 0, 1}
+                               : tail_plan(int64_t(s_pref[p.E]) * NT, int(gridDim.x), KT);
+  const int64_t total = plan.full + int64_t(plan.r) * plan.s;
   if (tid == 0) s_claim[0] = atomicAdd(p.queue, 1);
   __syncthreads();
 
@@ -194,20 +197,19 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
     const int64_t L = s_claim[it & 1];
     if (L >= total) break;
     if (tid == 0) s_claim[(it + 1) & 1] = atomicAdd(p.queue, 1);
-    const int e = __builtin_amdgcn_readfirstlane(find_expert(s_pref, p.E, L / NT));
-    const int pe = __builtin_amdgcn_readfirstlane(s_pref[e]);
-    const int mt_e = __builtin_amdgcn_readfirstlane(s_pref[e + 1]) - pe;
-    const int64_t local = L - int64_t(pe) * NT;
-    const int64_t bsz = int64_t(kGroupM) * NT;
-    const int mbi = int(local / bsz);
-    const int rem = int(local - int64_t(mbi) * bsz);
-    const int bm = min(kGroupM, mt_e - mbi * kGroupM);
-    const int ng = rem / (bm * kGroupN);
-    const int rem2 = rem - ng * bm * kGroupN;
-    const int mt = mbi * kGroupM + rem2 % bm;
-    const int nt = ng * kGroupN + rem2 / bm;
-    const int row0 = __builtin_amdgcn_readfirstlane(s_off[e]) + mt * kBM;
-    const int row_end = __builtin_amdgcn_readfirstlane(s_off[e + 1]);
+    // a whole tile, or piece j of a tail tile (k steps kt0..kt1, partial slot)
+    int64_t Lt = L;
+    int kt0 = 0, kt1 = KT, slot = -1;
+    if (L >= plan.full) {
+      const int q = int(L - plan.full);
+      const int j = q % plan.s;
+      Lt = plan.full + q / plan.s;
+      kt0 = j * KT / plan.s;
+      kt1 = (j + 1) * KT / plan.s;
+      slot = q;
+    }
+    const TileCoord tc = decode_tile(Lt, s_pref, s_off, p.E, NT);
+    const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_end = tc.row_end;
 
     const int arows = min(kBM, row_end - row0);
     const int n0 = SWIGLU ? nt * 128 : nt * 256;
@@ -358,17 +360,17 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
-      if (kt + 1 < KT) issue(nxt, kt + 1);
+      if (kt + 1 < kt1) issue(nxt, kt + 1);
       if (active) compute(cur);
     };
 
-    issue(st0, 0);
-    int kt = 0;
-    for (; kt + 2 <= KT; kt += 2) {
+    issue(st0, kt0);
+    int kt = kt0;
+    for (; kt + 2 <= kt1; kt += 2) {
       step(st0, st1, kt);
       step(st1, st0, kt + 1);
     }
-    if (kt < KT) step(st0, st1, kt);
+    if (kt < kt1) step(st0, st1, kt);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
 
@@ -400,6 +402,23 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
           if (khalf == 0) {
             const int b = f0 / 32;
             p.h_scales[(int64_t(b / 4) * p.R + row) * 4 + (b & 3)] = uint8_t(se + 127);
+          }
+        }
+      } else if (row < row_end && slot >= 0) {
+        // a piece of a tail tile: fp32 partial sums in its slot, tile-local
+        // [256 rows][256 columns], added in piece order by the tail reduction
+        float* prow = p.partial + (int64_t(slot) * kBM + (row - row0)) * kTileCols;
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+#pragma unroll
+          for (int blk = 0; blk < 4; ++blk) {
+            const int c = wn * 64 + ni * 32 + blk * 8 + khalf * 4;
+            if (n0 + c < N) {
+              f32x4 v;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) v[q] = acc[mi][ni][blk * 4 + q];
+              *reinterpret_cast<f32x4*>(prow + c) = v;
+            }
           }
         }
       } else if (row < row_end) {
@@ -441,22 +460,24 @@ hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* 
                             const int32_t* offsets, int64_t R, int E, int H, int F, const uint8_t* wg,
                             const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus, const uint8_t* wd,
                             const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint8_t* h,
-                            uint8_t* hs, int num_cu, hipStream_t s) {
+                            uint8_t* hs, float* partial, int num_cu, hipStream_t s) {
   hipError_t err = launch_tile_prefix(offsets, E, kBM, mtile_prefix, queues, s);
   if (err != hipSuccess) return err;
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
-  GemmArgsF8 a1{queues, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, offsets, mtile_prefix,
+  GemmArgsF8 a1{queues, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, nullptr, offsets, mtile_prefix,
                 E, H, F, F / 128, int(R), int(T)};
   const dim3 grid1(grid_for(mtiles_upper * a1.ntiles, num_cu));
   if (gather != nullptr)
     MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_fp8_kernel<true, true>), grid1, dim3(kThreads), s, a1);
   else
     MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_fp8_kernel<true, false>), grid1, dim3(kThreads), s, a1);
-  GemmArgsF8 a2{queues + 1, h, hs, nullptr, wd, wds, nullptr, nullptr, nullptr, nullptr, y_perm, offsets,
+  GemmArgsF8 a2{queues + 1, h, hs, nullptr, wd, wds, nullptr, nullptr, nullptr, nullptr, y_perm, partial, offsets,
                 mtile_prefix, E, F, H, (H + 255) / 256, int(R), 0};
-  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_fp8_kernel<false, false>),
-             dim3(grid_for(mtiles_upper * a2.ntiles, num_cu)), dim3(kThreads), s, a2);
-  return hipGetLastError();
+  const int grid2 = grid_for(mtiles_upper * a2.ntiles, num_cu);
+  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_fp8_kernel<false, false>), dim3(grid2), dim3(kThreads), s, a2);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  return launch_tail_reduce(partial, mtile_prefix, offsets, E, a2.ntiles, grid2, F / kBK, H, y_perm, s);
 }
 
 }  // namespace moe

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
+#include <atomic>
 #include <mutex>
 #include <string>
 
@@ -28,9 +29,16 @@ moe_status hip_status(const char* fn, hipError_t err) {
   return MOE_ERR_HIP;
 }
 
-// Compute units of the current device, cached per device (the persistent GEMM
-// grid is sized from it).
+std::atomic<int> g_cu_budget{0};
+
+// Compute units the persistent grids are sized for: the budget set with
+// moe_set_cu_budget, else the current device's count (cached per device).
 int cu_count(hipError_t* err) {
+  const int budget = g_cu_budget.load(std::memory_order_relaxed);
+  if (budget > 0) {
+    *err = hipSuccess;
+    return budget;
+  }
   static std::mutex mu;
   static int cache[64] = {0};
   int dev = 0;
@@ -54,6 +62,17 @@ hipStream_t stream_of(moe_stream s) { return reinterpret_cast<hipStream_t>(s); }
 extern "C" {
 
 int moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+moe_status moe_set_cu_budget(int32_t n) {
+  moe::Check c;
+  if (n < 0) {
+    c.status = MOE_ERR_INVALID_ARGUMENT;
+    c.msg = "moe_set_cu_budget: n=" + std::to_string(n) + " is negative";
+    return finish(c);
+  }
+  g_cu_budget.store(n, std::memory_order_relaxed);
+  return finish(c);
+}
 
 const char* moe_status_string(int status) {
   switch (status) {
@@ -135,13 +154,12 @@ moe_status run_ffn(const char* fn, const void* act, const int32_t* gather, int64
   hipError_t err;
   const int ncu = cu_count(&err);
   if (err != hipSuccess) return hip_status(fn, err);
-  const int ksplit = moe::ffn_down_ksplit(R, E, H, F, dt);
   auto* partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + moe::ffn_partial_offset(R, E, F, dt));
   return hip_status(
       fn, moe::launch_ffn_bf16(static_cast<const uint16_t*>(act), gather, T, expert_offsets, R, E, H, F,
                                static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
                                static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), prefix,
-                               queues, static_cast<uint16_t*>(h), partial, ksplit, ncu, stream_of(stream)));
+                               queues, static_cast<uint16_t*>(h), partial, ncu, stream_of(stream)));
 }
 
 }  // namespace
@@ -202,9 +220,10 @@ moe_status run_ffn_mxfp8(const char* fn, const uint8_t* x_codes, const uint8_t* 
   auto* queues = reinterpret_cast<int32_t*>(base + moe::ffn_queue_offset(E));
   uint8_t* h = base + moe::ffn_h_offset(E);
   uint8_t* hs = base + moe::ffn_mxfp8_h_scales_offset(R, E, F);
+  auto* partial = reinterpret_cast<float*>(base + moe::ffn_mxfp8_partial_offset(R, E, F));
   return hip_status(fn, moe::launch_ffn_mxfp8(x_codes, x_scales, gather, T, expert_offsets, R, E, H, F, wg_codes,
                                               wg_scales, wu_codes, wu_scales, wd_codes, wd_scales,
-                                              static_cast<uint16_t*>(y_perm), prefix, queues, h, hs, ncu,
+                                              static_cast<uint16_t*>(y_perm), prefix, queues, h, hs, partial, ncu,
                                               stream_of(stream)));
 }
 

@@ -34,12 +34,17 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
 
 // Grouped SwiGLU FFN (bf16).  act is x_perm [R, H], or with gather != null the
 // token rows x [T, H] read through gather[r] (T * H * 2 < 2^31).  Device scratch:
-// mtile_prefix (E + 1 ints), queues (2 ints), h [R, F], and partial [ksplit, R, H]
-// fp32 when ksplit > 1; all are rewritten by the call before use.
+// mtile_prefix (E + 1 ints), queues (2 ints), h [R, F], and the down
+// projection's tail-split partial slots (ffn_tail_partial_bytes); all are
+// rewritten by the call before use.
 hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T, const int32_t* offsets,
                            int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
-                           uint16_t* h, float* partial, int ksplit, int num_cu, hipStream_t s);
+                           uint16_t* h, float* partial, int num_cu, hipStream_t s);
+// Sums the tail-split pieces of a down projection (G workgroups, KT k steps,
+// NT n-tiles of 256 over N columns) into y; a no-op launch when the plan has none.
+hipError_t launch_tail_reduce(const float* partial, const int32_t* mtile_prefix, const int32_t* offsets, int E,
+                              int NT, int G, int KT, int N, uint16_t* y, hipStream_t s);
 // Per-expert m-tile prefix of the device-side offsets (one block); zeroes the
 // GEMMs' tile-queue counters when queues != null.
 hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
@@ -49,14 +54,15 @@ hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mt
 // [K / 128][rows_out][4]; output row r reads source row row_map[r] (or r).
 hipError_t launch_quantize_mxfp8(const uint16_t* src, const int32_t* row_map, int64_t rows_out, int K,
                                  uint8_t* codes, uint8_t* scales, int num_cu, hipStream_t s);
-// Grouped SwiGLU FFN on MXFP8 operands; h (MXFP8, R x F codes + scales) is device
-// scratch.  x is the grouped rows [R, H], or with gather != null the token rows
-// [T, H] read through gather[r] (T * H < 2^31).
+// Grouped SwiGLU FFN on MXFP8 operands; h (MXFP8, R x F codes + scales) and the
+// down projection's tail-split partial slots are device scratch.  x is the
+// grouped rows [R, H], or with gather != null the token rows [T, H] read through
+// gather[r] (T * H < 2^31).
 hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* gather, int64_t T,
                             const int32_t* offsets, int64_t R, int E, int H, int F, const uint8_t* wg,
                             const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus, const uint8_t* wd,
                             const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint8_t* h,
-                            uint8_t* hs, int num_cu, hipStream_t s);
+                            uint8_t* hs, float* partial, int num_cu, hipStream_t s);
 
 hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
                           int E, int H, int F, const float* wg, const float* wu, const float* wd,

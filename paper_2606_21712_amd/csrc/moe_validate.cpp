@@ -1,5 +1,6 @@
 // Host-side argument validation (no HIP calls); see moe_validate.h.
 #include "moe_validate.h"
+#include "tiling.h"
 
 #include <climits>
 #include <cstdio>
@@ -90,24 +91,22 @@ size_t permute_workspace_bytes(int64_t T, int32_t E, int32_t k) {
 size_t ffn_queue_offset(int32_t E) { return align256(size_t(E + 1) * sizeof(int32_t)); }
 size_t ffn_h_offset(int32_t E) { return ffn_queue_offset(E) + 256; }
 
-int ffn_down_ksplit(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt) {
-  if (dt != MOE_DTYPE_BF16 || R <= 0 || E < 1) return 1;
-  // Upper bound of the down projection's 256 x 256 output tiles.  Below three
-  // rounds of 256 compute units, and with a long k (>= 64 steps of 64), the k
-  // range is split in two so the last round is not mostly idle.
-  const int64_t mtiles = (R + int64_t(E) * 255) / 256;
-  const int64_t tiles = mtiles * ((H + 255) / 256);
-  return (tiles < 3 * 256 && F / 64 >= 64) ? 2 : 1;
-}
-
 size_t ffn_partial_offset(int64_t R, int32_t E, int32_t F, moe_dtype dt) {
   return ffn_h_offset(E) + align256(size_t(R) * size_t(F) * elt(dt));
 }
 
+size_t ffn_tail_partial_bytes(int64_t R, int32_t E, int32_t H, int32_t F, int bk) {
+  if (R <= 0 || E < 1 || H < 1 || F / bk < 2 * kMinPieceSteps) return 0;
+  // The grid never exceeds the output-tile bound, and the pieces never exceed the grid.
+  const int64_t mtiles = (R + int64_t(E) * (kTileRows - 1)) / kTileRows;
+  const int64_t tiles = mtiles * ((H + kTileCols - 1) / kTileCols);
+  const int64_t slots = tiles < kMaxTailPieces ? tiles : kMaxTailPieces;
+  return size_t(slots) * kTileRows * kTileCols * sizeof(float);
+}
+
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt) {
   if (R <= 0 || E < 1 || F < 1) return 0;
-  const int ks = ffn_down_ksplit(R, E, H, F, dt);
-  const size_t partial = ks > 1 ? align256(size_t(ks) * size_t(R) * size_t(H) * sizeof(float)) : 0;
+  const size_t partial = dt == MOE_DTYPE_BF16 ? ffn_tail_partial_bytes(R, E, H, F, 64) : 0;
   return ffn_partial_offset(R, E, F, dt) + partial;
 }
 
@@ -250,9 +249,13 @@ size_t ffn_mxfp8_h_scales_offset(int64_t R, int32_t E, int32_t F) {
   return ffn_h_offset(E) + align256(size_t(R) * size_t(F));
 }
 
+size_t ffn_mxfp8_partial_offset(int64_t R, int32_t E, int32_t F) {
+  return ffn_mxfp8_h_scales_offset(R, E, F) + align256(mxfp8_scale_bytes(R, F));
+}
+
 size_t ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F) {
   if (R <= 0 || E < 1 || F < 1 || H < 1) return 0;
-  return ffn_mxfp8_h_scales_offset(R, E, F) + align256(mxfp8_scale_bytes(R, F));
+  return ffn_mxfp8_partial_offset(R, E, F) + ffn_tail_partial_bytes(R, E, H, F, 128);
 }
 
 Check validate_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t rows_out, int64_t rows_src,

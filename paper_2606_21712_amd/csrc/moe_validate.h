@@ -20,11 +20,14 @@ struct Check {
 size_t permute_workspace_bytes(int64_t T, int32_t E, int32_t k);
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt);
 // ffn workspace: [m-tile prefix (E + 1 ints) | tile queues | h [R, F] |
-//                 down-projection partials [ksplit, R, H] fp32 when ksplit > 1]
+//                 down-projection tail-split partial slots]
 size_t ffn_queue_offset(int32_t E);
 size_t ffn_h_offset(int32_t E);
 size_t ffn_partial_offset(int64_t R, int32_t E, int32_t F, moe_dtype dt);
-int ffn_down_ksplit(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt);
+// Partial slots of the down projection's tail split: 256 x 256 fp32 each, at most
+// kMaxTailPieces and at most the output-tile bound; none when the k loop (F / bk
+// steps) is too short to split.
+size_t ffn_tail_partial_bytes(int64_t R, int32_t E, int32_t H, int32_t F, int bk);
 int64_t permute_units(int64_t R);           // count-units (1024 assignments each)
 
 constexpr int64_t kPermuteUnit = 1024;      // assignments per counting unit (one wavefront)
@@ -43,10 +46,11 @@ Check validate_ffn_gather(const void* x, const int32_t* sorted_tok, int64_t T, c
                           int64_t R, int32_t E, int32_t H, int32_t F, const void* wg, const void* wu,
                           const void* wd, int dt, const void* y_perm, const void* ws, size_t ws_bytes);
 // MXFP8: scales of a [rows, K] matrix; ffn workspace [prefix | queues | h codes
-// [R, F] | h scales]
+// [R, F] | h scales | down-projection tail-split partial slots]
 size_t mxfp8_scale_bytes(int64_t rows, int32_t K);
 size_t ffn_mxfp8_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F);
 size_t ffn_mxfp8_h_scales_offset(int64_t R, int32_t E, int32_t F);
+size_t ffn_mxfp8_partial_offset(int64_t R, int32_t E, int32_t F);
 Check validate_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t rows_out, int64_t rows_src,
                               int32_t K, const void* codes, const void* scales);
 Check validate_ffn_mxfp8(const void* x, const void* xs, const int32_t* offsets, int64_t R, int32_t E, int32_t H,

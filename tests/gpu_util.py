@@ -55,3 +55,49 @@ def rel_max_err(gpu: np.ndarray, ref: np.ndarray) -> float:
     if scale == 0:
         return float(np.abs(gpu).max())
     return float(np.abs(gpu - ref).max() / scale)
+
+
+# The grouped GEMMs' tail split (the down projection's last, partly filled round
+# of 256 x 256 output tiles cut along k), restated for choosing test cases:
+# n tiles on G persistent workgroups with KT k steps each.
+MAX_TAIL_PIECES, MAX_TAIL_SPLIT, MIN_PIECE_STEPS = 256, 8, 8
+
+
+def tail_plan(n: int, G: int, KT: int):
+    """(full, r, s): tiles [0, full) whole, the r after them in s pieces each."""
+    if G < 2:
+        return n, 0, 1
+    r = n % G
+    if r == 0 or 2 * r > G:
+        return n, 0, 1
+    s = min(min(G, MAX_TAIL_PIECES) // r, KT // MIN_PIECE_STEPS, MAX_TAIL_SPLIT)
+    if s < 2:
+        return n, 0, 1
+    return n - r, r, s
+
+
+def down_tiles(offsets: np.ndarray, H: int) -> tuple[int, int]:
+    """(actual, upper bound) of the down projection's 256 x 256 output tiles."""
+    counts = np.diff(np.asarray(offsets, dtype=np.int64))
+    nt = (H + 255) // 256
+    actual = int(((counts + 255) // 256).sum()) * nt
+    upper = (int(counts.sum()) + len(counts) * 255) // 256 * nt
+    return actual, upper
+
+
+def split_budgets(offsets: np.ndarray, H: int, KT: int, want: int = 3):
+    """Compute-unit budgets under which the down projection splits its tail, with
+    distinct (r, s); plus one under which it does not (None if there is none)."""
+    n, upper = down_tiles(offsets, H)
+    cands, seen, plain = [], set(), None
+    for b in range(2, upper + 1):
+        full, r, s = tail_plan(n, min(b, upper), KT)
+        if r == 0:
+            plain = b if plain is None else plain
+        elif (r, s) not in seen:
+            seen.add((r, s))
+            cands.append((b, r, s))
+    # spread over the range: the smallest, the largest and evenly between
+    if len(cands) > want:
+        cands = [cands[round(i * (len(cands) - 1) / (want - 1))] for i in range(want)]
+    return cands, plain

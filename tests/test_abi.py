@@ -99,10 +99,20 @@ def test_ffn_validation(L):
     assert ffn(L, R=0, xp=None, off=None, wg=None, wu=None, wd=None, yp=None, ws=None, ws_bytes=0) == 0
     # fp32 h is twice as large
     assert L.moe_grouped_ffn_workspace_bytes(100, 8, 128, 256, 0) > need
-    # few output tiles with a long k: room for two fp32 partials of the down projection
+    # the down projection's tail split: one 256 x 256 fp32 slot per possible output
+    # tile (E * 255 + R rows in 256-row tiles, times H / 256), at most 256 slots
     R, H, F = 2048, 256, 4096
-    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, F, 1) >= R * F * 2 + 2 * R * H * 4
-    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, 1024, 1) < R * 1024 * 2 + R * H * 4
+    slot = 256 * 256 * 4
+    tiles = (R + 8 * 255) // 256 * (H // 256)
+    need = L.moe_grouped_ffn_workspace_bytes(R, 8, H, F, 1)
+    assert R * F * 2 + tiles * slot <= need < R * F * 2 + (tiles + 1) * slot
+    big = L.moe_grouped_ffn_workspace_bytes(1 << 20, 8, 4096, F, 1)
+    assert (1 << 20) * F * 2 + 256 * slot <= big < (1 << 20) * F * 2 + 257 * slot
+    # a k loop too short to cut in two pieces of 8 steps (F / 64 < 16): no slots
+    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, 1024, 1) >= R * 1024 * 2 + tiles * slot
+    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, 960, 1) < R * 960 * 2 + slot
+    # fp32 has no tail split
+    assert L.moe_grouped_ffn_workspace_bytes(R, 8, H, F, 0) < R * F * 4 + slot
 
 
 def ffn_gather(L, x=P, st=P, off=P, T=50, R=100, E=8, H=128, F=256, wg=P, wu=P, wd=P, dt=1, yp=P, ws=P,
@@ -163,7 +173,11 @@ def test_ffn_mxfp8_validation(L):
     assert ffn8(L, xs=P + 8) == INVALID
     need = L.moe_grouped_ffn_mxfp8_workspace_bytes(100, 8, 128, 256)
     assert need >= 100 * 256 + 100 * 256 // 32                   # h codes + scales
+    assert need < 100 * 256 * 2                                   # k loop of 2 steps: no tail split
     assert ffn8(L, ws_bytes=need - 1) == WS_SMALL
+    # k loop of 16 steps of 128: tail-split slots of 256 x 256 fp32 per possible output tile
+    tiles = (100 + 8 * 255) // 256
+    assert L.moe_grouped_ffn_mxfp8_workspace_bytes(100, 8, 256, 2048) >= 100 * 2048 + tiles * 256 * 256 * 4
     assert ffn8(L, R=0, x=None, xs=None, off=None, wg=None, wgs=None, wu=None, wus=None, wd=None, wds=None,
                 yp=None, ws=None, ws_bytes=0) == 0
 
@@ -222,6 +236,13 @@ def test_combine_validation(L):
     assert combine(L, y=None) == INVALID
     assert combine(L, ys=P + 4) == INVALID
     assert combine(L, T=0, yp=None, dest=None, w=None, y=None) == 0
+
+
+def test_cu_budget_validation(L):
+    assert L.moe_set_cu_budget(-1) == INVALID
+    assert b"moe_set_cu_budget" in L.moe_last_error()
+    assert L.moe_set_cu_budget(7) == 0
+    assert L.moe_set_cu_budget(0) == 0
 
 
 def test_binding_rejects_cpu_tensors():

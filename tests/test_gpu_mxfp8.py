@@ -230,6 +230,38 @@ def test_layer_mxfp8(name):
     assert rel_max_err(f64(to_host(layer.y)), ref["y"]) <= 0.1
 
 
+def test_mxfp8_down_projection_tail_split():
+    """MXFP8 down projection with its last round of tiles cut along k (planned for fewer
+    compute units): h is untouched (GEMM-1 never splits), y_perm outside the tail
+    keeps its bits and the tail moves only by reassociation; y_perm still meets the
+    per-element bound against the kernel's own h."""
+    from tests.gpu_util import split_budgets
+    from tests.test_gpu_parity import check_tail_split
+    c = moegen.MoEConfig("f8_tail_split", T=2048, H=512, E=8, k=2, F=4096, seed=35)
+    I = moegen.make_inputs(c)
+    ref = mxfp8.layer_mxfp8(I.x, I.logits, c.k, I.w_gate, I.w_up, I.w_down, 1)
+    picks, plain = split_budgets(ref["offsets"], c.H, c.F // 128)
+    assert len(picks) >= 2 and plain is not None, (picks, plain)
+    try:
+        log(f"[gpu] mxfp8 tail split reference: budget {plain}, no split")
+        moe.set_cu_budget(plain)
+        base, _ = run_mxfp8_layer(c, I)
+        h_base = to_host(base.ws_ffn)
+        y_base = to_host(base.y_perm)
+        xd = mxfp8.dequantize_mxfp8(ref["x_codes"], ref["x_scales"])[ref["sorted_token_ids"]]
+        for b, r, s in picks:
+            log(f"[gpu] mxfp8 tail split: budget {b}, {r} tail tiles in {s} pieces")
+            moe.set_cu_budget(b)
+            g, _ = run_mxfp8_layer(c, I)
+            hb = c.T * c.k * c.F
+            h_off = ((c.E + 1) * 4 + 255) // 256 * 256 + 256
+            assert np.array_equal(to_host(g.ws_ffn)[h_off:h_off + hb], h_base[h_off:h_off + hb])
+            check_tail_split(to_host(g.y_perm), y_base, r, f"budget {b}")
+            check_ffn(xd, ref["offsets"], I.w_gate, I.w_up, I.w_down, g.ws_ffn, g.y_perm, f"budget {b}")
+    finally:
+        moe.set_cu_budget(0)
+
+
 def test_layer_mxfp8_gather_equals_grouped_copy():
     """Gathering the token codes in GEMM-1 gives the same bits as quantizing x into
     grouped order first."""

@@ -11,7 +11,7 @@ import torch
 import moegen
 import oracle
 import paper_2606_21712_amd as moe
-from tests.gpu_util import f64, log, rel_max_err, to_dev, to_host, weight_tol
+from tests.gpu_util import f64, log, rel_max_err, split_budgets, to_dev, to_host, weight_tol
 
 pytestmark = pytest.mark.gpu
 
@@ -37,7 +37,7 @@ CASES = {
     "k_eq_E": small("k_eq_E", T=260, H=64, E=4, k=4, F=64, seed=17),
     "T1": small("T1", T=1, H=64, E=8, k=2, F=64, seed=18),
     "H64_f32": small("H64_f32", T=333, H=64, E=5, k=2, F=64, seed=19, dtype="f32"),
-    # few down-projection tiles and a long k: the down projection splits k in two
+    # few down-projection tiles and a long k (224 steps of 64)
     "ksplit_small": small("ksplit_small", T=1024, H=256, E=8, k=2, F=4096, seed=20),
 }
 
@@ -99,6 +99,47 @@ def test_layer_parity(name):
     err = rel_max_err(f64(g["y"]), o["y"])
     log(f"[gpu]   max|dy|/max|y| = {err:.3e}")
     assert err <= tol
+
+
+def check_tail_split(y_split, y_whole, r, label):
+    """A run whose down projection cut r tail tiles along k against one that ran every
+    tile whole: at most r tiles' elements differ, each by fp32 reassociation of the
+    pieces' partial sums plus one bf16 rounding (2^-7 relative, and 2^-16 of the
+    largest output for values that cancel)."""
+    a, b = f64(y_split), f64(y_whole)
+    n_diff = int((y_split != y_whole).sum())
+    log(f"[gpu]   {label}: {n_diff} elements differ from the unsplit run (limit {r * 256 * 256})")
+    assert n_diff <= r * 256 * 256
+    assert (np.abs(a - b) <= 2.0 ** -7 * np.abs(b) + 2.0 ** -16 * np.abs(b).max()).all()
+
+
+def test_down_projection_tail_split():
+    """The last, partly filled round of down-projection tiles cut along k, reached at a
+    small size by planning the grid for fewer compute units: tiles outside the tail
+    keep their bits, tail tiles move only by reassociation, y_perm stays within the
+    oracle bar per expert group."""
+    c = small("tail_split", T=2048, H=512, E=8, k=2, F=2048, seed=21)
+    I = moegen.make_inputs(c)
+    o = oracle_layer(I)
+    picks, plain = split_budgets(o["offsets"], c.H, c.F // 64)
+    assert len(picks) >= 2 and plain is not None, (picks, plain)
+    try:
+        log(f"[gpu] tail split reference: budget {plain}, no split")
+        moe.set_cu_budget(plain)
+        base = run_layer(I)
+        for b, r, s in picks:
+            log(f"[gpu] tail split: budget {b}, {r} tail tiles in {s} pieces")
+            moe.set_cu_budget(b)
+            g = run_layer(I)
+            check_tail_split(g["y_perm"], base["y_perm"], r, f"budget {b}")
+            yp = f64(g["y_perm"])
+            for e in range(c.E):
+                lo, hi = o["offsets"][e], o["offsets"][e + 1]
+                if hi > lo:
+                    assert rel_max_err(yp[lo:hi], o["y_perm"][lo:hi]) <= BF16_TOL, (b, e)
+            assert rel_max_err(f64(g["y"]), o["y"]) <= BF16_TOL
+    finally:
+        moe.set_cu_budget(0)
 
 
 @pytest.mark.parametrize("name", ["tiny_f32", "mixtral_small", "zipf_small", "deepseek_small", "memc_small",
