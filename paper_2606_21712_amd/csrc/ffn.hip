@@ -346,8 +346,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
 }
 
 // Tail tiles of a down projection: y = bf16(sum of the tile's piece partials, in
-// piece order).  One block per tail tile (blocks past the plan's r exit); G and KT
-// are the GEMM's grid size and k steps, so the plan is the GEMM's own.
+// piece order).  kTailStrips blocks per tail tile, each 256 / kTailStrips rows of
+// it; blocks past the plan's r tiles exit.  G and KT are the GEMM's grid size and
+// k steps, so the plan is the GEMM's own.  A thread issues the loads of all its
+// pieces before adding them (latency, not bandwidth, bounds a strip).
+constexpr int kTailStrips = 16;
+
 __global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restrict__ partial,
                                                          const int32_t* __restrict__ mtile_prefix,
                                                          const int32_t* __restrict__ offsets, int E, int NT, int G,
@@ -360,28 +364,40 @@ __global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restric
   }
   __syncthreads();
   const TailPlan plan = tail_plan(int64_t(s_pref[E]) * NT, G, KT);
-  if (int(blockIdx.x) >= plan.r) return;                       // uniform across the block
-  const TileCoord tc = decode_tile(plan.full + blockIdx.x, s_pref, s_off, E, NT);
+  const int t = int(blockIdx.x) / kTailStrips;
+  if (t >= plan.r) return;                                     // uniform across the block
+  const TileCoord tc = decode_tile(plan.full + t, s_pref, s_off, E, NT);
   const int rows = min(kTileRows, tc.row_end - tc.row0);
   const int n0 = tc.nt * kTileCols;
   const int cols = min(kTileCols, N - n0);
-  const float* base = partial + int64_t(blockIdx.x) * plan.s * (kTileRows * kTileCols);
-  // 8 consecutive columns per item; a row is 32 items
-  for (int i = threadIdx.x; i < rows * (kTileCols / 8); i += blockDim.x) {
-    const int r = i / (kTileCols / 8);
+  // this block's strip: rows r0 .. r0 + 15; 8 consecutive columns per item, 32 items a row
+  constexpr int kStripRows = kTileRows / kTailStrips;
+  const int r0 = (int(blockIdx.x) % kTailStrips) * kStripRows;
+  const float* base = partial + int64_t(t) * plan.s * (kTileRows * kTileCols);
+  for (int i = threadIdx.x; i < kStripRows * (kTileCols / 8); i += blockDim.x) {
+    const int r = r0 + i / (kTileCols / 8);
     const int c = (i % (kTileCols / 8)) * 8;
-    if (c >= cols) continue;
+    if (r >= rows || c >= cols) continue;
+    f32x4 v[kMaxTailSplit][2];
+#pragma unroll
+    for (int j = 0; j < kMaxTailSplit; ++j) {
+      if (j < plan.s) {
+        const f32x4* src = reinterpret_cast<const f32x4*>(base + (int64_t(j) * kTileRows + r) * kTileCols + c);
+        v[j][0] = __builtin_nontemporal_load(src);
+        v[j][1] = __builtin_nontemporal_load(src + 1);
+      }
+    }
     float acc[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[q] = 0.f;
-    for (int j = 0; j < plan.s; ++j) {
-      const f32x4* src = reinterpret_cast<const f32x4*>(base + (int64_t(j) * kTileRows + r) * kTileCols + c);
-      const f32x4 a = __builtin_nontemporal_load(src);
-      const f32x4 b = __builtin_nontemporal_load(src + 1);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[q] += a[q];
-        acc[4 + q] += b[q];
+    for (int j = 0; j < kMaxTailSplit; ++j) {
+      if (j < plan.s) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[q] += v[j][0][q];
+          acc[4 + q] += v[j][1][q];
+        }
       }
     }
     u32x4 pk;
@@ -490,7 +506,7 @@ hipError_t launch_tail_reduce(const float* partial, const int32_t* mtile_prefix,
   // A split happens only with at least two pieces of kMinPieceSteps steps; then
   // r <= min(G, kMaxTailPieces) / 2 tail tiles.
   if (KT < 2 * kMinPieceSteps || G < 2) return hipSuccess;
-  const int blocks = std::min(G, kMaxTailPieces) / 2;
+  const int blocks = std::min(G, kMaxTailPieces) / 2 * kTailStrips;
   MOE_LAUNCH("ffn_tail_reduce", tail_reduce_kernel, dim3(unsigned(blocks)), dim3(256), s, partial, mtile_prefix,
              offsets, E, NT, G, KT, N, y);
   return hipGetLastError();
