@@ -304,10 +304,15 @@ moe_status moe_combine(const void* y_perm, const int32_t* dest_rows, const float
  * only allocation, and it happens here, not in the layer calls.  After the
  * caller synchronizes, moe_profiler_record(i, &name, &ms) returns the i-th
  * launch's kernel name (a static string) and its duration in milliseconds.
+ * moe_profiler_select(name) restricts recording to launches of the kernel of
+ * that name (as moe_profiler_record reports it, e.g. "ffn_gemm1_gate_up"), so
+ * that timing one kernel leaves the others' launches untouched; NULL or ""
+ * records every launch again.  It applies to launches made after the call.
  * Errors: INVALID_ARGUMENT for capacity < 1 or an index out of range; HIP for
  * an event failure (e.g. the record's stream has not completed).
  */
 moe_status moe_profiler_start(int capacity);
+moe_status moe_profiler_select(const char* name);
 moe_status moe_profiler_stop(void);
 int moe_profiler_count(void);
 moe_status moe_profiler_record(int i, const char** name, float* ms);

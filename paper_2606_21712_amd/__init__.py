@@ -22,7 +22,7 @@ __all__ = [
     "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
     "moe_grouped_ffn_mxfp8", "moe_grouped_ffn_mxfp8_gather", "MXFP8", "quantize_weights_mxfp8",
     "MoELayerMXFP8",
-    "profiler_start", "profiler_stop", "profiler_records", "set_cu_budget",
+    "profiler_start", "profiler_select", "profiler_stop", "profiler_records", "set_cu_budget",
     "DTYPE_F32", "DTYPE_BF16",
 ]
 
@@ -71,6 +71,7 @@ _SIGNATURES = {
     "moe_grouped_ffn_mxfp8_gather": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P,
                                                     _P, _P, _P, _P, _SZ, _P]),
     "moe_profiler_start": (ctypes.c_int, [ctypes.c_int]),
+    "moe_profiler_select": (ctypes.c_int, [ctypes.c_char_p]),
     "moe_set_cu_budget": (ctypes.c_int, [_I32]),
     "moe_profiler_stop": (ctypes.c_int, []),
     "moe_profiler_count": (ctypes.c_int, []),
@@ -349,6 +350,11 @@ def set_cu_budget(n: int = 0):
 def profiler_start(capacity: int = 4096):
     """Bracket every following kernel launch of the library with HIP events."""
     _check(lib().moe_profiler_start(capacity))
+
+
+def profiler_select(name=None):
+    """Record only launches of the kernel `name` (None: every launch)."""
+    _check(lib().moe_profiler_select(name.encode() if name else None))
 
 
 def profiler_stop():

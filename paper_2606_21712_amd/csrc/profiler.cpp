@@ -1,12 +1,14 @@
 // Optional per-kernel timing with HIP events (a benchmarking aid).
 //
-// When enabled, every kernel the library launches is bracketed by a pair of
-// events recorded on the launch stream.  Event pairs come from a pool created
-// by moe_profiler_start(), so recording adds no allocation to the hot path.
-// When disabled (the default) a launch pays one relaxed atomic load.
+// When enabled, every kernel the library launches (or only those of one name,
+// after moe_profiler_select) is bracketed by a pair of events recorded on the
+// launch stream.  Event pairs come from a pool created by moe_profiler_start(),
+// so recording adds no allocation to the hot path.  When disabled (the
+// default) a launch pays one relaxed atomic load.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cstring>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -26,6 +28,7 @@ std::atomic<bool> g_on{false};
 std::mutex g_mu;
 std::vector<Rec> g_pool;   // created by start(), destroyed by the next start()
 size_t g_used = 0;
+std::string g_only;        // record only launches of this name ("" = all)
 thread_local Rec* g_open = nullptr;
 
 }  // namespace
@@ -34,6 +37,7 @@ void prof_begin(hipStream_t s, const char* name) {
   if (!g_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lock(g_mu);
   if (g_used >= g_pool.size()) return;
+  if (!g_only.empty() && std::strcmp(name, g_only.c_str()) != 0) return;
   Rec* r = &g_pool[g_used++];
   r->name = name;
   hipEventRecord(r->a, s);
@@ -67,6 +71,12 @@ moe_status moe_profiler_start(int capacity) {
     if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return MOE_ERR_HIP;
   }
   g_on.store(true);
+  return MOE_OK;
+}
+
+moe_status moe_profiler_select(const char* name) {
+  std::lock_guard<std::mutex> lock(moe::g_mu);
+  moe::g_only = name != nullptr ? name : "";
   return MOE_OK;
 }
 
