@@ -75,12 +75,22 @@ constexpr int kGroupM = 4;
 struct TileCoord {
   int e;          // expert
   int row0;       // first grouped row of the tile
-  int row_end;    // end of the expert's rows (the tile covers [row0, min(row0 + 256, row_end)))
+  int row_stop;   // end of the tile's rows: row0 + 256, or the expert's end for its last m-tile
   int nt;         // n-tile index
 };
 
+// m-tiles of an expert with c rows: ceil(c / 256), or with extra > 0 the count
+// that lets the last tile take up to 256 + extra rows.
+__host__ __device__ __forceinline__ int mtiles_of(int c, int extra) {
+  if (c <= 0) return 0;
+  const int rest = c - extra;
+  return rest <= 0 ? 1 : (rest + kTileRows - 1) / kTileRows;
+}
+
 // Tile L of the list; pref/off are the m-tile prefix and row offsets (E + 1
-// entries, typically staged in LDS).  All lanes pass the same L.
+// entries, typically staged in LDS).  All lanes pass the same L.  The last
+// m-tile of an expert ends at the expert's end (at most 256 + the extra rows
+// the prefix was built with), every other one after 256 rows.
 __device__ __forceinline__ TileCoord decode_tile(int64_t L, const int32_t* pref, const int32_t* off, int E,
                                                  int NT) {
   TileCoord t;
@@ -97,7 +107,8 @@ __device__ __forceinline__ TileCoord decode_tile(int64_t L, const int32_t* pref,
   const int mt = mbi * kGroupM + rem2 % bm;
   t.nt = ng * kGroupN + rem2 / bm;
   t.row0 = __builtin_amdgcn_readfirstlane(off[t.e]) + mt * kTileRows;
-  t.row_end = __builtin_amdgcn_readfirstlane(off[t.e + 1]);
+  const int row_end = __builtin_amdgcn_readfirstlane(off[t.e + 1]);
+  t.row_stop = mt == mt_e - 1 ? row_end : t.row0 + kTileRows;
   return t;
 }
 

@@ -30,6 +30,7 @@
 // are free of bank conflicts; operand fragments are double-buffered in
 // registers so LDS latency hides behind the previous sub-step's MFMAs.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "moe_internal.h"
@@ -40,16 +41,18 @@ namespace {
 // ----------------------------------------------------------------------------- tile prefix
 constexpr int kQueueInts = 2;             // tile counters: GEMM-1's, then GEMM-2's
 
-// prefix[e] = sum_{e' < e} ceil(count[e'] / bm), prefix[E] = total.  One block of 256.
+// prefix[e] = sum_{e' < e} m-tiles of expert e', prefix[E] = total: ceil(count / bm)
+// m-tiles, or (bm = 256, extra > 0) the count whose last tile takes up to 256 +
+// extra rows.  One block of 256.
 __global__ __launch_bounds__(256) void tile_prefix_kernel(const int32_t* __restrict__ offsets, int E,
-                                                         int bm, int32_t* __restrict__ prefix,
+                                                         int bm, int extra, int32_t* __restrict__ prefix,
                                                          int32_t* __restrict__ queues) {
   const int e = threadIdx.x;
   if (queues != nullptr && e < kQueueInts) queues[e] = 0;      // tile queues of both GEMMs
   int32_t mt = 0;
   if (e < E) {
     const int32_t c = offsets[e + 1] - offsets[e];
-    mt = (c + bm - 1) / bm;
+    mt = extra > 0 ? mtiles_of(c, extra) : (c + bm - 1) / bm;
   }
   int32_t total;
   const int32_t ex = block_exclusive_scan256(mt, &total);
@@ -58,12 +61,15 @@ __global__ __launch_bounds__(256) void tile_prefix_kernel(const int32_t* __restr
 }
 
 // ----------------------------------------------------------------------------- bf16 MFMA GEMM
-constexpr int kBM = 256;                  // activation rows per tile
+constexpr int kBM = 256;                  // activation rows per m-tile (an expert's last: up to kBMMax)
+constexpr int kBMMax = kTileRowsMax;      // 320
 constexpr int kBN = 256;                  // weight rows per tile (GEMM-1: 128 gate + 128 up)
 constexpr int kBK = 64;                   // k per pipeline step
 constexpr int kRowBytes = kBK * 2;        // one tile row in LDS: 128 bytes = 8 chunks of 16
-constexpr int kOpBytes = 256 * kRowBytes; // one operand tile: 32 KB
-constexpr int kStageBytes = 2 * kOpBytes;
+constexpr int kWOpBytes = kBN * kRowBytes;       // weight tile: 32 KB
+constexpr int kAOpBytes = kBMMax * kRowBytes;    // activation tile: 40 KB
+constexpr int kStageBytes = kWOpBytes + kAOpBytes;
+constexpr int kWaveRows = kBMMax / 2;     // 160 activation rows per wavefront: 5 blocks of 32
 constexpr int kGemmThreads = 512;        // 8 wavefronts: 2 (m) x 4 (n), two per SIMD
 static_assert(kBM == kTileRows && kBN == kTileCols, "tile shape");
 
@@ -145,8 +151,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   if (tid == 0) s_claim[0] = atomicAdd(p.queue, 1);
   __syncthreads();
 
-  // DMA: wave w's pass i fills the 1 KB block blk = 8*i + w (tile rows 8*blk..8*blk+7);
-  // lane q lands at byte 16*q of the block: row 8*blk + q/8, chunk position q%8.
+  // DMA: wave w's pass i fills the 1 KB block blk = 8*i + w of an operand (its rows
+  // 8*blk..8*blk+7); lane q lands at byte 16*q of the block: row 8*blk + q/8, chunk
+  // position q%8.  Weights: 32 blocks (4 passes); activations: 40 blocks (5 passes).
   const int qrow = lane >> 3;
   const int qpos = lane & 7;
   // MFMA operand reads: row (lane % 32) of a 32-row block, k-chunk 2*s + lane / 32.
@@ -170,11 +177,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
       slot = q;
     }
     const TileCoord tc = decode_tile(Lt, s_pref, s_off, p.E, NT);
-    const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_end = tc.row_end;
+    const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_stop = tc.row_stop;
+    const int arows = row_stop - row0;                           // 1 .. 320
 
-    // ---- buffer resources: rows past the group end (activations) or past N
-    // (weights) fall outside num_records and load as zeros.
-    const int arows = min(kBM, row_end - row0);
+    // ---- buffer resources: rows past the tile (activations) or past N (weights)
+    // fall outside num_records and load as zeros.
     const int n0 = SWIGLU ? nt * 128 : nt * 256;
     const int wrows = SWIGLU ? min(128, N - n0) : min(256, N - n0);
     const int64_t rowb = int64_t(K) * 2;
@@ -187,23 +194,28 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
         const_cast<uint16_t*>(p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
     const __amdgpu_buffer_rsrc_t rw1 = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(SWIGLU ? p.w1 : p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
-    // Per-lane byte offsets of the 4 DMA passes per operand (constant over the k loop).
-    uint32_t aoff[4], woff[4];
+    // Per-lane byte offsets of the DMA passes (constant over the k loop).
+    uint32_t aoff[5], woff[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = (8 * i + wave) * 8 + qrow;                  // tile row this lane fills
+    for (int i = 0; i < 5; ++i) {
+      const int r = (8 * i + wave) * 8 + qrow;                  // activation row this lane fills
       const uint32_t cb = uint32_t(swz(r, qpos) * 16);          // its logical chunk, in bytes
       if (GATHER) {
-        // The token's row; rows past the group end get an offset beyond num_records.
+        // The token's row; rows past the tile get an offset beyond num_records.
         const int grow = row0 + r;
-        aoff[i] = grow < row_end ? uint32_t(p.gather[grow]) * uint32_t(rowb) + cb : 0x80000000u;
+        aoff[i] = grow < row_stop ? uint32_t(p.gather[grow]) * uint32_t(rowb) + cb : 0x80000000u;
       } else {
         aoff[i] = uint32_t(r) * uint32_t(rowb) + cb;
       }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = (8 * i + wave) * 8 + qrow;
+      const uint32_t cb = uint32_t(swz(r, qpos) * 16);
       // GEMM-1: tile rows 0..127 are gate features n0.., rows 128..255 the same up features.
       woff[i] = uint32_t(SWIGLU ? (r & 127) : r) * uint32_t(rowb) + cb;
     }
-
+    // Activation passes whose 8 rows all lie past the tile are not issued.
     auto issue = [&](uint8_t* stage, int kt) {
       const int kb = kt * kRowBytes;
 #pragma unroll
@@ -211,87 +223,112 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
         const int blk = 8 * i + wave;
         __builtin_amdgcn_raw_ptr_buffer_load_lds((SWIGLU && i >= 2) ? rw1 : rw0, stage + blk * 1024, 16,
                                                  woff[i], kb, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 5; ++i) {
+        const int blk = 8 * i + wave;
+        if (blk * 8 < arows)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kWOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
       }
     };
 
-    f32x16 acc[4][2];
+    f32x16 acc[5][2];
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < 5; ++mi)
 #pragma unroll
       for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[mi][ni][q] = 0.f;
 
-    auto frags = [&](const uint8_t* stage, int s, bf16x8* wf, bf16x8* xf) {
-      const int c = 2 * s + khalf;
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int row = wave_nrow<SWIGLU>(wn, ni) + rrow;
-        wf[ni] = *reinterpret_cast<const bf16x8*>(stage + row * kRowBytes + swz(row, c) * 16);
-      }
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
-        const int row = wm * 128 + mi * 32 + rrow;
-        xf[mi] = *reinterpret_cast<const bf16x8*>(stage + kOpBytes + row * kRowBytes + swz(row, c) * 16);
-      }
-    };
-    auto compute = [&](const uint8_t* stage) {
-      bf16x8 wf[2][2], xf[2][4];
-      frags(stage, 0, wf[0], xf[0]);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s < 3) frags(stage, s + 1, wf[(s + 1) & 1], xf[(s + 1) & 1]);
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < 2; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s & 1][ni], xf[s & 1][mi],
-                                                                  acc[mi][ni], 0, 0, 0);
-        // Issue order: the next sub-step's 6 LDS reads spread between this one's MFMAs.
-        if (s < 3) {
-#pragma unroll
-          for (int i = 0; i < 6; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-          }
-          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        } else {
-          __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-        }
-      }
-    };
-    // One k-step: wait for this stage's loads (own lanes, then all waves via the
-    // barrier, which also frees the other stage), start the next step's loads into
-    // the other stage, then run the MFMAs of this one.
-    // A wavefront whose 128 rows all lie past the group end (the tail m-tile of
-    // a group) still loads and synchronizes but skips its MFMAs: the other wave
-    // on its SIMD then has the matrix core to itself.
-    const bool active = row0 + wm * 128 < row_end;
-    auto step = [&](uint8_t* cur, uint8_t* nxt, int kt) {
-      __builtin_amdgcn_sched_barrier(0);
-      __builtin_amdgcn_s_waitcnt(kWaitVm0);
-      __syncthreads();
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + 1 < kt1) issue(nxt, kt + 1);
-      if (active) compute(cur);
-    };
+    // This wavefront's rows: wm * 160 + 32 mi + (lane % 32); NB of its five 32-row
+    // blocks hold rows of the tile (0 for the second wavefront row of a short tile:
+    // it still loads and synchronizes, and the other wave on its SIMD has the
+    // matrix core to itself).
+    const int nb = min(5, max(0, (arows - wm * kWaveRows + 31) / 32));
 
-    issue(st0, kt0);
-    int kt = kt0;
-    for (; kt + 2 <= kt1; kt += 2) {
-      step(st0, st1, kt);
-      step(st1, st0, kt + 1);
+    // One k-loop per block count, so the fragment reads and MFMAs of a step are a
+    // fixed unrolled sequence.
+    auto kloop = [&](auto nb_c) {
+      constexpr int NB = decltype(nb_c)::value;
+      auto frags = [&](const uint8_t* stage, int s, bf16x8* wf, bf16x8* xf) {
+        const int c = 2 * s + khalf;
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+          const int row = wave_nrow<SWIGLU>(wn, ni) + rrow;
+          wf[ni] = *reinterpret_cast<const bf16x8*>(stage + row * kRowBytes + swz(row, c) * 16);
+        }
+#pragma unroll
+        for (int mi = 0; mi < NB; ++mi) {
+          const int row = wm * kWaveRows + mi * 32 + rrow;
+          xf[mi] = *reinterpret_cast<const bf16x8*>(stage + kWOpBytes + row * kRowBytes + swz(row, c) * 16);
+        }
+      };
+      auto compute = [&](const uint8_t* stage) {
+        if constexpr (NB > 0) {
+          bf16x8 wf[2][2], xf[2][NB];
+          frags(stage, 0, wf[0], xf[0]);
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            if (s < 3) frags(stage, s + 1, wf[(s + 1) & 1], xf[(s + 1) & 1]);
+#pragma unroll
+            for (int mi = 0; mi < NB; ++mi)
+#pragma unroll
+              for (int ni = 0; ni < 2; ++ni)
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s & 1][ni], xf[s & 1][mi],
+                                                                      acc[mi][ni], 0, 0, 0);
+            // Issue order: the next sub-step's 2 + NB LDS reads spread between this
+            // one's 2 NB MFMAs.
+            if (s < 3) {
+              constexpr int kReads = 2 + NB, kMfmas = 2 * NB;
+              constexpr int kPairs = kReads < kMfmas ? kReads : kMfmas;
+#pragma unroll
+              for (int i = 0; i < kPairs; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+              }
+              if constexpr (kMfmas > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfmas - kPairs, 0);
+              if constexpr (kReads > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPairs, 0);
+            } else {
+              __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+            }
+          }
+        }
+      };
+      // One k-step: wait for this stage's loads (own lanes, then all waves via the
+      // barrier, which also frees the other stage), start the next step's loads
+      // into the other stage, then run the MFMAs of this one.
+      auto step = [&](uint8_t* cur, uint8_t* nxt, int kt) {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 1 < kt1) issue(nxt, kt + 1);
+        compute(cur);
+      };
+      issue(st0, kt0);
+      int kt = kt0;
+      for (; kt + 2 <= kt1; kt += 2) {
+        step(st0, st1, kt);
+        step(st1, st0, kt + 1);
+      }
+      if (kt < kt1) step(st0, st1, kt);
+    };
+    switch (nb) {
+      case 5: kloop(std::integral_constant<int, 5>{}); break;
+      case 4: kloop(std::integral_constant<int, 4>{}); break;
+      case 3: kloop(std::integral_constant<int, 3>{}); break;
+      case 2: kloop(std::integral_constant<int, 2>{}); break;
+      case 1: kloop(std::integral_constant<int, 1>{}); break;
+      default: kloop(std::integral_constant<int, 0>{}); break;
     }
-    if (kt < kt1) step(st0, st1, kt);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();              // every wave is done with both stages before the next tile
 
     // ---- epilogue: lane holds columns n + 8*blk + 4*khalf + {0..3} of row (lane % 32)
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
-      const int row = row0 + wm * 128 + mi * 32 + rrow;
-      if (row < row_end) {
+    for (int mi = 0; mi < 5; ++mi) {
+      const int row = row0 + wm * kWaveRows + mi * 32 + rrow;
+      if (row < row_stop) {
         uint16_t* orow = p.out + int64_t(row) * N;
         if (SWIGLU) {
 #pragma unroll
@@ -310,8 +347,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
           }
         } else if (slot >= 0) {
           // A piece of a tail tile: fp32 partial sums in its slot, tile-local
-          // [256 rows][256 columns], added in piece order by tail_reduce_kernel.
-          float* prow = p.partial + (int64_t(slot) * kBM + (row - row0)) * kBN;
+          // [320 rows][256 columns], added in piece order by tail_reduce_kernel.
+          float* prow = p.partial + (int64_t(slot) * kBMMax + (row - row0)) * kBN;
 #pragma unroll
           for (int ni = 0; ni < 2; ++ni) {
 #pragma unroll
@@ -367,13 +404,13 @@ __global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restric
   const int t = int(blockIdx.x) / kTailStrips;
   if (t >= plan.r) return;                                     // uniform across the block
   const TileCoord tc = decode_tile(plan.full + t, s_pref, s_off, E, NT);
-  const int rows = min(kTileRows, tc.row_end - tc.row0);
+  const int rows = tc.row_stop - tc.row0;
   const int n0 = tc.nt * kTileCols;
   const int cols = min(kTileCols, N - n0);
-  // this block's strip: rows r0 .. r0 + 15; 8 consecutive columns per item, 32 items a row
-  constexpr int kStripRows = kTileRows / kTailStrips;
+  // this block's strip: rows r0 .. r0 + 19; 8 consecutive columns per item, 32 items a row
+  constexpr int kStripRows = kTileRowsMax / kTailStrips;
   const int r0 = (int(blockIdx.x) % kTailStrips) * kStripRows;
-  const float* base = partial + int64_t(t) * plan.s * (kTileRows * kTileCols);
+  const float* base = partial + int64_t(t) * plan.s * (kTileRowsMax * kTileCols);
   for (int i = threadIdx.x; i < kStripRows * (kTileCols / 8); i += blockDim.x) {
     const int r = r0 + i / (kTileCols / 8);
     const int c = (i % (kTileCols / 8)) * 8;
@@ -382,7 +419,7 @@ __global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restric
 #pragma unroll
     for (int j = 0; j < kMaxTailSplit; ++j) {
       if (j < plan.s) {
-        const f32x4* src = reinterpret_cast<const f32x4*>(base + (int64_t(j) * kTileRows + r) * kTileCols + c);
+        const f32x4* src = reinterpret_cast<const f32x4*>(base + (int64_t(j) * kTileRowsMax + r) * kTileCols + c);
         v[j][0] = __builtin_nontemporal_load(src);
         v[j][1] = __builtin_nontemporal_load(src + 1);
       }
@@ -512,9 +549,10 @@ hipError_t launch_tail_reduce(const float* partial, const int32_t* mtile_prefix,
   return hipGetLastError();
 }
 
-hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
-                              hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, bm, mtile_prefix, queues);
+hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int extra, int32_t* mtile_prefix,
+                              int32_t* queues, hipStream_t s) {
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, bm, extra, mtile_prefix,
+             queues);
   return hipGetLastError();
 }
 
@@ -522,8 +560,8 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
                            int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
                            uint16_t* h, float* partial, int num_cu, hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, mtile_prefix,
-             queues);
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, kTileExtraRows,
+             mtile_prefix, queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
   GemmArgs a1{queues, act, gather, wg, wu, h, nullptr, offsets, mtile_prefix, E, H, F, (F + 127) / 128,
@@ -547,7 +585,7 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
 hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
                           int E, int H, int F, const float* wg, const float* wu, const float* wd,
                           float* y_perm, int32_t* mtile_prefix, float* h, hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, mtile_prefix,
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, 0, mtile_prefix,
              static_cast<int32_t*>(nullptr));
   const int64_t mtiles_upper = (R + int64_t(E) * (kFM - 1)) / kFM;
   GemmArgsF a1{act, gather, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + kFN - 1) / kFN};

@@ -209,9 +209,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
       slot = q;
     }
     const TileCoord tc = decode_tile(Lt, s_pref, s_off, p.E, NT);
-    const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_end = tc.row_end;
+    const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_stop = tc.row_stop;
 
-    const int arows = min(kBM, row_end - row0);
+    const int arows = min(kBM, row_stop - row0);
     const int n0 = SWIGLU ? nt * 128 : nt * 256;
     const int wrows = SWIGLU ? min(128, N - n0) : min(256, N - n0);
     const __amdgpu_buffer_rsrc_t ra =
@@ -241,7 +241,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
       if (GATHER) {
         // the token's row; rows past the group end get an offset beyond num_records
         const int grow = row0 + r;
-        aoff[i] = grow < row_end ? uint32_t(p.gather[grow]) * uint32_t(K) + cb : 0x80000000u;
+        aoff[i] = grow < row_stop ? uint32_t(p.gather[grow]) * uint32_t(K) + cb : 0x80000000u;
       } else {
         aoff[i] = uint32_t(r) * uint32_t(K) + cb;
       }
@@ -253,7 +253,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int grow = row0 + 64 * j + lane;
-      stok[j] = (GATHER && wave == 1 && grow < row_end) ? uint32_t(p.gather[grow]) * 4u : 0x80000000u;
+      stok[j] = (GATHER && wave == 1 && grow < row_stop) ? uint32_t(p.gather[grow]) * 4u : 0x80000000u;
     }
     // scale rows: wave 0 loads the weight tile's 256 scale dwords (GEMM-1: lanes
     // 0-31 the 128 gate rows, lanes 32-63 the up rows), wave 1 the activation tile's
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
         }
       }
     };
-    const bool active = row0 + wm * 128 < row_end;
+    const bool active = row0 + wm * 128 < row_stop;
     auto step = [&](uint8_t* cur, uint8_t* nxt, int kt) {
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
@@ -389,7 +389,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
         }
         amax = fmaxf(amax, __shfl_xor(amax, 32));
         const int f0 = n0 + wn * 32;                           // block start, a multiple of 32
-        if (row < row_end && f0 < N) {
+        if (row < row_stop && f0 < N) {
           const int se = mx_shared_exp(amax);
           const float inv = mx_inv_scale(se);
           uint8_t* crow = p.h_codes + int64_t(row) * N + f0 + khalf * 4;
@@ -404,10 +404,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
             p.h_scales[(int64_t(b / 4) * p.R + row) * 4 + (b & 3)] = uint8_t(se + 127);
           }
         }
-      } else if (row < row_end && slot >= 0) {
+      } else if (row < row_stop && slot >= 0) {
         // a piece of a tail tile: fp32 partial sums in its slot, tile-local
         // [256 rows][256 columns], added in piece order by the tail reduction
-        float* prow = p.partial + (int64_t(slot) * kBM + (row - row0)) * kTileCols;
+        float* prow = p.partial + (int64_t(slot) * kTileRowsMax + (row - row0)) * kTileCols;
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) {
 #pragma unroll
@@ -421,7 +421,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
             }
           }
         }
-      } else if (row < row_end) {
+      } else if (row < row_stop) {
         uint16_t* orow = p.y + int64_t(row) * N;
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) {
@@ -461,7 +461,7 @@ hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* 
                             const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus, const uint8_t* wd,
                             const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint8_t* h,
                             uint8_t* hs, float* partial, int num_cu, hipStream_t s) {
-  hipError_t err = launch_tile_prefix(offsets, E, kBM, mtile_prefix, queues, s);
+  hipError_t err = launch_tile_prefix(offsets, E, kBM, 0, mtile_prefix, queues, s);
   if (err != hipSuccess) return err;
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
   GemmArgsF8 a1{queues, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, nullptr, offsets, mtile_prefix,

@@ -97,11 +97,12 @@ size_t ffn_partial_offset(int64_t R, int32_t E, int32_t F, moe_dtype dt) {
 
 size_t ffn_tail_partial_bytes(int64_t R, int32_t E, int32_t H, int32_t F, int bk) {
   if (R <= 0 || E < 1 || H < 1 || F / bk < 2 * kMinPieceSteps) return 0;
-  // The grid never exceeds the output-tile bound, and the pieces never exceed the grid.
+  // The grid never exceeds the output-tile bound, and the pieces never exceed the grid;
+  // a slot holds a tile of up to kTileRowsMax rows.
   const int64_t mtiles = (R + int64_t(E) * (kTileRows - 1)) / kTileRows;
   const int64_t tiles = mtiles * ((H + kTileCols - 1) / kTileCols);
   const int64_t slots = tiles < kMaxTailPieces ? tiles : kMaxTailPieces;
-  return size_t(slots) * kTileRows * kTileCols * sizeof(float);
+  return size_t(slots) * kTileRowsMax * kTileCols * sizeof(float);
 }
 
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt) {

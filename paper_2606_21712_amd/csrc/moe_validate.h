@@ -24,7 +24,7 @@ size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype
 size_t ffn_queue_offset(int32_t E);
 size_t ffn_h_offset(int32_t E);
 size_t ffn_partial_offset(int64_t R, int32_t E, int32_t F, moe_dtype dt);
-// Partial slots of the down projection's tail split: 256 x 256 fp32 each, at most
+// Partial slots of the down projection's tail split: 320 x 256 fp32 each, at most
 // kMaxTailPieces and at most the output-tile bound; none when the k loop (F / bk
 // steps) is too short to split.
 size_t ffn_tail_partial_bytes(int64_t R, int32_t E, int32_t H, int32_t F, int bk);

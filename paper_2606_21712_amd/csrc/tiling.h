@@ -5,9 +5,14 @@
 namespace moe {
 
 // Output tiles of the grouped GEMMs are 256 x 256 (GEMM-1: 256 rows x 128
-// features of both gate and up).
+// features of both gate and up).  An expert's rows are cut into m-tiles of
+// kTileRows; in the bf16 GEMMs the last one may hold up to kTileRows +
+// kTileExtraRows rows, so that a remainder of at most kTileExtraRows rows joins
+// the tile before it instead of costing a tile of its own.
 constexpr int kTileRows = 256;
 constexpr int kTileCols = 256;
+constexpr int kTileExtraRows = 64;
+constexpr int kTileRowsMax = kTileRows + kTileExtraRows;
 
 // Tail split of the down projection.  A persistent grid of G workgroups runs
 // n output tiles in ceil(n / G) rounds; the last holds only r = n mod G tiles.

@@ -76,19 +76,28 @@ def tail_plan(n: int, G: int, KT: int):
     return n - r, r, s
 
 
-def down_tiles(offsets: np.ndarray, H: int) -> tuple[int, int]:
-    """(actual, upper bound) of the down projection's 256 x 256 output tiles."""
+def mtiles(counts, extra: int) -> np.ndarray:
+    """m-tiles per expert: 256-row tiles, the last taking up to 256 + extra rows."""
+    c = np.asarray(counts, dtype=np.int64)
+    rest = np.maximum(c - extra, 0)
+    return np.where(c == 0, 0, np.maximum(1, (rest + 255) // 256))
+
+
+def down_tiles(offsets: np.ndarray, H: int, extra: int) -> tuple[int, int]:
+    """(actual, upper bound) of the down projection's output tiles (256 columns;
+    extra = 64 for the bf16 GEMMs, whose last m-tile of an expert takes up to 320
+    rows, 0 for the MXFP8 ones)."""
     counts = np.diff(np.asarray(offsets, dtype=np.int64))
     nt = (H + 255) // 256
-    actual = int(((counts + 255) // 256).sum()) * nt
+    actual = int(mtiles(counts, extra).sum()) * nt
     upper = (int(counts.sum()) + len(counts) * 255) // 256 * nt
     return actual, upper
 
 
-def split_budgets(offsets: np.ndarray, H: int, KT: int, want: int = 3):
+def split_budgets(offsets: np.ndarray, H: int, KT: int, extra: int, want: int = 3):
     """Compute-unit budgets under which the down projection splits its tail, with
     distinct (r, s); plus one under which it does not (None if there is none)."""
-    n, upper = down_tiles(offsets, H)
+    n, upper = down_tiles(offsets, H, extra)
     cands, seen, plain = [], set(), None
     for b in range(2, upper + 1):
         full, r, s = tail_plan(n, min(b, upper), KT)

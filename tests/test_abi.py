@@ -99,10 +99,10 @@ def test_ffn_validation(L):
     assert ffn(L, R=0, xp=None, off=None, wg=None, wu=None, wd=None, yp=None, ws=None, ws_bytes=0) == 0
     # fp32 h is twice as large
     assert L.moe_grouped_ffn_workspace_bytes(100, 8, 128, 256, 0) > need
-    # the down projection's tail split: one 256 x 256 fp32 slot per possible output
+    # the down projection's tail split: one 320 x 256 fp32 slot per possible output
     # tile (E * 255 + R rows in 256-row tiles, times H / 256), at most 256 slots
     R, H, F = 2048, 256, 4096
-    slot = 256 * 256 * 4
+    slot = 320 * 256 * 4                    # a tile of up to 320 rows x 256 columns, fp32
     tiles = (R + 8 * 255) // 256 * (H // 256)
     need = L.moe_grouped_ffn_workspace_bytes(R, 8, H, F, 1)
     assert R * F * 2 + tiles * slot <= need < R * F * 2 + (tiles + 1) * slot
@@ -175,9 +175,9 @@ def test_ffn_mxfp8_validation(L):
     assert need >= 100 * 256 + 100 * 256 // 32                   # h codes + scales
     assert need < 100 * 256 * 2                                   # k loop of 2 steps: no tail split
     assert ffn8(L, ws_bytes=need - 1) == WS_SMALL
-    # k loop of 16 steps of 128: tail-split slots of 256 x 256 fp32 per possible output tile
+    # k loop of 16 steps of 128: tail-split slots of 320 x 256 fp32 per possible output tile
     tiles = (100 + 8 * 255) // 256
-    assert L.moe_grouped_ffn_mxfp8_workspace_bytes(100, 8, 256, 2048) >= 100 * 2048 + tiles * 256 * 256 * 4
+    assert L.moe_grouped_ffn_mxfp8_workspace_bytes(100, 8, 256, 2048) >= 100 * 2048 + tiles * 320 * 256 * 4
     assert ffn8(L, R=0, x=None, xs=None, off=None, wg=None, wgs=None, wu=None, wus=None, wd=None, wds=None,
                 yp=None, ws=None, ws_bytes=0) == 0
 

@@ -240,7 +240,7 @@ def test_mxfp8_down_projection_tail_split():
     c = moegen.MoEConfig("f8_tail_split", T=2048, H=512, E=8, k=2, F=4096, seed=35)
     I = moegen.make_inputs(c)
     ref = mxfp8.layer_mxfp8(I.x, I.logits, c.k, I.w_gate, I.w_up, I.w_down, 1)
-    picks, plain = split_budgets(ref["offsets"], c.H, c.F // 128)
+    picks, plain = split_budgets(ref["offsets"], c.H, c.F // 128, 0)
     assert len(picks) >= 2 and plain is not None, (picks, plain)
     try:
         log(f"[gpu] mxfp8 tail split reference: budget {plain}, no split")

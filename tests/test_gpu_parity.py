@@ -38,7 +38,7 @@ CASES = {
     "T1": small("T1", T=1, H=64, E=8, k=2, F=64, seed=18),
     "H64_f32": small("H64_f32", T=333, H=64, E=5, k=2, F=64, seed=19, dtype="f32"),
     # few down-projection tiles and a long k (224 steps of 64)
-    "ksplit_small": small("ksplit_small", T=1024, H=256, E=8, k=2, F=4096, seed=20),
+    "longk_small": small("longk_small", T=1024, H=256, E=8, k=2, F=4096, seed=20),
 }
 
 
@@ -101,6 +101,50 @@ def test_layer_parity(name):
     assert err <= tol
 
 
+# Group sizes around the m-tile edges: an expert's last m-tile holds up to 320 rows
+# (256 + 64), so 257..320 rows make one tile, 321 two, 576 two (256 + 320), 577
+# three; plus 1, 64, 65 and an empty expert.
+EDGE_COUNTS = [256, 257, 300, 320, 321, 512, 576, 577, 1, 64, 65, 0]
+
+
+def edge_count_inputs(H=256, F=320, seed=22):
+    """k = 1 inputs whose routing gives exactly EDGE_COUNTS rows per expert: each
+    token's logit for its expert is 8 above the others (router noise is ~0.3)."""
+    E = len(EDGE_COUNTS)
+    T = sum(EDGE_COUNTS)
+    I = moegen.make_inputs(small("edge_counts", T=T, H=H, E=E, k=1, F=F, seed=seed))
+    rng = np.random.default_rng(seed)
+    expert = rng.permutation(np.repeat(np.arange(E), EDGE_COUNTS))
+    logits = I.logits.copy()
+    logits[np.arange(T), expert] += np.float32(8.0)
+    I.logits = logits
+    return I, expert
+
+
+def test_last_m_tile_extra_rows():
+    """Groups whose sizes sit on the m-tile edges (including the 320-row last tile)
+    against the oracle, through the copy and the gather paths (bitwise equal)."""
+    I, expert = edge_count_inputs()
+    c = I.cfg
+    log(f"[gpu] edge group sizes {EDGE_COUNTS}: T={c.T} H={c.H} F={c.F}")
+    o = oracle_layer(I)
+    assert np.array_equal(o["counts"], np.array(EDGE_COUNTS))
+    assert np.array_equal(o["ids"][:, 0], expert)
+    g = run_layer(I)
+    b = run_layer(I, gather=True)
+    assert np.array_equal(g["ids"], o["ids"])
+    assert np.array_equal(g["offsets"], o["offsets"])
+    yp = f64(g["y_perm"])
+    for e in range(c.E):
+        lo, hi = o["offsets"][e], o["offsets"][e + 1]
+        if hi > lo:
+            err = rel_max_err(yp[lo:hi], o["y_perm"][lo:hi])
+            assert err <= BF16_TOL, (e, hi - lo, err)
+    assert rel_max_err(f64(g["y"]), o["y"]) <= BF16_TOL
+    assert np.array_equal(g["y_perm"], b["y_perm"])
+    assert np.array_equal(g["y"], b["y"])
+
+
 def check_tail_split(y_split, y_whole, r, label):
     """A run whose down projection cut r tail tiles along k against one that ran every
     tile whole: at most r tiles' elements differ, each by fp32 reassociation of the
@@ -121,7 +165,7 @@ def test_down_projection_tail_split():
     c = small("tail_split", T=2048, H=512, E=8, k=2, F=2048, seed=21)
     I = moegen.make_inputs(c)
     o = oracle_layer(I)
-    picks, plain = split_budgets(o["offsets"], c.H, c.F // 64)
+    picks, plain = split_budgets(o["offsets"], c.H, c.F // 64, 64)
     assert len(picks) >= 2 and plain is not None, (picks, plain)
     try:
         log(f"[gpu] tail split reference: budget {plain}, no split")
@@ -143,7 +187,7 @@ def test_down_projection_tail_split():
 
 
 @pytest.mark.parametrize("name", ["tiny_f32", "mixtral_small", "zipf_small", "deepseek_small", "memc_small",
-                                  "uniform_router", "T1", "ksplit_small", "H64_f32"])
+                                  "uniform_router", "T1", "longk_small", "H64_f32"])
 def test_gather_path_matches_grouped_path(name):
     """moe_grouped_ffn_gather gives bit-for-bit the y_perm of moe_grouped_ffn on x_perm,
     and the layer output stays within the oracle bar."""
