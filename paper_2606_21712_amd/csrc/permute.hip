@@ -6,7 +6,8 @@
 // holding the same expert find each other with 8 ballots over the id bits (a
 // match mask); a lane's rank among equal experts is the popcount of the match
 // mask below it, so the order inside an expert group is the assignment order,
-// i.e. ascending token.  Four kernels, no atomics:
+// i.e. ascending token.  Four kernels, no atomics (batches of at most 16 units
+// run the first three as one single-block kernel):
 //   count : per-unit, per-expert counts                      -> uc[E][units]
 //   scan  : per expert, exclusive scan over units; totals    -> uc, counts
 //   rank  : offsets = exclusive scan of counts; every assignment's row
@@ -116,6 +117,90 @@ __global__ __launch_bounds__(kThreads) void permute_rank_kernel(
   }
 }
 
+// Small batches (at most kSmallUnits units): the three phases in one block of
+// 1024 threads, one wavefront per unit, with the per-unit counts in LDS.  Same
+// results as count + scan + rank.
+constexpr int kSmallUnits = 16;
+constexpr int kSmallThreads = kSmallUnits * kWave;
+
+__global__ __launch_bounds__(kSmallThreads) void permute_small_kernel(
+    const int32_t* __restrict__ ids, int64_t R, int E, int k, int nbits, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ dest, int32_t* __restrict__ sorted_tok) {
+  __shared__ int32_t run[kSmallUnits][kMaxExperts];
+  __shared__ int32_t s_wsum[4];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int w = tid / kWave;                                // the unit
+  const int64_t base = int64_t(w) * kUnit;
+  const uint64_t below = (1ull << lane) - 1ull;
+  // the unit's ids, all loaded at once and kept for the rank phase
+  int idv[kIters];
+#pragma unroll
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t a = base + it * kWave + lane;
+    idv[it] = a < R ? ids[a] : -1;
+  }
+  for (int e = lane; e < E; e += kWave) run[w][e] = 0;
+  __syncthreads();
+  // counts per unit
+#pragma unroll
+  for (int it = 0; it < kIters; ++it) {
+    const bool valid = idv[it] >= 0;
+    const int id = valid ? idv[it] : 0;
+    const uint64_t match = wave_match(id, valid, nbits);
+    if (valid && (match & below) == 0ull) run[w][id] += __popcll(match);
+  }
+  __syncthreads();
+  // per expert: exclusive scan over the units, then offsets = exclusive scan of the
+  // totals over the experts (threads 0..255, one expert each)
+  int32_t total = 0;
+  if (tid < E) {
+    for (int u = 0; u < kSmallUnits; ++u) {
+      const int32_t c = run[u][tid];
+      run[u][tid] = total;
+      total += c;
+    }
+    counts[tid] = total;
+  }
+  int32_t x = total;                                          // inclusive scan over threads 0..255
+  if (tid < kMaxExperts) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int32_t y = __shfl_up(x, d);
+      if (lane >= d) x += y;
+    }
+    if (lane == kWave - 1) s_wsum[w] = x;
+  }
+  __syncthreads();
+  if (tid < kMaxExperts) {
+    int32_t before = 0;
+    for (int i = 0; i < w; ++i) before += s_wsum[i];
+    const int32_t ex = before + x - total;                   // exclusive offset of expert tid
+    if (tid < E) {
+      offsets[tid] = ex;
+      for (int u = 0; u < kSmallUnits; ++u) run[u][tid] += ex;
+    }
+    if (tid == E - 1) offsets[E] = ex + total;
+  }
+  __syncthreads();
+  // rows: the unit's running position per expert plus the rank among equal ids
+#pragma unroll
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t a = base + it * kWave + lane;
+    const bool valid = idv[it] >= 0;
+    const int id = valid ? idv[it] : 0;
+    const uint64_t match = wave_match(id, valid, nbits);
+    if (valid) {
+      const int32_t r0 = run[w][id];
+      const int32_t rank = __popcll(match & below);
+      const int32_t row = r0 + rank;
+      dest[a] = row;
+      sorted_tok[row] = int32_t(uint32_t(a) / uint32_t(k));
+      if (rank == 0) run[w][id] = r0 + __popcll(match);
+    }
+  }
+}
+
 template <int UNROLL>
 __global__ __launch_bounds__(kThreads) void permute_copy_kernel(const uint8_t* __restrict__ x,
                                                                int64_t T, int k, int64_t row_bytes,
@@ -156,12 +241,17 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
   const int64_t U = (R + kUnit - 1) / kUnit;
   int nbits = 0;
   while ((1 << nbits) < E) ++nbits;
-  const unsigned unit_blocks = unsigned(Upad / kWavesPerBlock);
-  MOE_LAUNCH("permute_count", permute_count_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E,
-             nbits, Upad, uc);
-  MOE_LAUNCH("permute_scan", permute_scan_kernel, dim3(E), dim3(kThreads), s, uc, U, Upad, counts);
-  MOE_LAUNCH("permute_rank", permute_rank_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E, k,
-             nbits, Upad, uc, counts, offsets, dest, sorted_tok);
+  if (U <= kSmallUnits) {
+    MOE_LAUNCH("permute_small", permute_small_kernel, dim3(1), dim3(kSmallThreads), s, ids, R, E, k, nbits,
+               counts, offsets, dest, sorted_tok);
+  } else {
+    const unsigned unit_blocks = unsigned(Upad / kWavesPerBlock);
+    MOE_LAUNCH("permute_count", permute_count_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E,
+               nbits, Upad, uc);
+    MOE_LAUNCH("permute_scan", permute_scan_kernel, dim3(E), dim3(kThreads), s, uc, U, Upad, counts);
+    MOE_LAUNCH("permute_rank", permute_rank_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E, k,
+               nbits, Upad, uc, counts, offsets, dest, sorted_tok);
+  }
   if (x_perm == nullptr) return hipGetLastError();     // maps only: the grouped FFN gathers rows
   const int64_t row_bytes = int64_t(H) * elt;
   const unsigned copy_blocks = unsigned((T + kWavesPerBlock - 1) / kWavesPerBlock);
