@@ -151,11 +151,16 @@ moe_status moe_permute(const int32_t* topk_ids, const void* x, int64_t T, int32_
  *   w_down          dt  [E, H, F]  K-contiguous
  *   y_perm          dt  [R, H]     out: W_down[e] (silu(W_gate[e] x) * (W_up[e] x))
  *   ws, ws_bytes    device scratch of at least moe_grouped_ffn_workspace_bytes();
- *                   it holds the intermediate h [R, F]
+ *                   it holds the intermediate h [R, F] and (bf16) fp32 partial
+ *                   sums of down-projection tiles split along k
  *
  * silu(z) = z / (1 + exp(-z)).  bf16: fp32 accumulation, h and y_perm rounded
  * to bf16 (nearest even).  f32: fp32 throughout.  Group sizes are read on the
- * device only (no host readback).
+ * device only (no host readback).  Results are deterministic for a given device
+ * and compute-unit budget (moe_set_cu_budget): when the last round of
+ * down-projection tiles would leave the grid mostly idle, those tiles are
+ * computed in pieces along k and their fp32 partial sums added in piece order,
+ * so their rounding depends on the grid size.
  * Errors: INVALID_ARGUMENT for R < 0, E < 1, H or F not a positive multiple of
  * 64, R > INT32_MAX, null or misaligned pointers; UNSUPPORTED for E > 256 or
  * an unknown dtype; WORKSPACE_TOO_SMALL.
@@ -234,12 +239,14 @@ moe_status moe_quantize_mxfp8(const void* src, const int32_t* row_map, int64_t r
  *   wd_*                 MXFP8 [E * H, F] W_down quantized along F
  *   y_perm               bf16 [R, H]     out
  *   ws, ws_bytes         device scratch of at least moe_grouped_ffn_mxfp8_workspace_bytes();
- *                        it holds h [R, F] in MXFP8
+ *                        it holds h [R, F] in MXFP8 and fp32 partial sums of
+ *                        down-projection tiles split along k
  *
  * g and u accumulate in fp32 from the dequantized operands (the matrix cores
  * apply the block scales), h = silu(g) * u in fp32 is quantized to MXFP8 along F
  * as moe_quantize_mxfp8 does, and y_perm accumulates in fp32 and is rounded to
- * bf16 (nearest even).
+ * bf16 (nearest even).  Determinism as moe_grouped_ffn: for a given device and
+ * compute-unit budget.
  * Errors: INVALID_ARGUMENT for R < 0, R > INT32_MAX, E < 1, H or F not a
  * positive multiple of 128, null or misaligned pointers; UNSUPPORTED for
  * E > 256 or when a scale array or an expert matrix reaches 2 GiB;

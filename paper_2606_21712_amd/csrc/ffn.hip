@@ -17,9 +17,13 @@
 // the last-level cache shared by all XCDs serves the panels better when the
 // whole GPU works on one compact front of the tile list.)
 //
-// bf16 tile: 256 rows x 256 weight rows x 64 k per step, 8 wavefronts (2 x 4,
-// two per SIMD so one issues MFMAs while the other waits), each a 128 x 64
-// block of v_mfma_f32_32x32x16_bf16 results (8 MFMA tiles).
+// bf16 tile: 256 rows (an expert's last m-tile up to 320) x 256 weight rows x
+// 64 k per step, 8 wavefronts (2 x 4, two per SIMD so one issues MFMAs while
+// the other waits), each up to 160 x 64: five 32-row blocks of
+// v_mfma_f32_32x32x16_bf16 results, of which a wavefront computes only those
+// holding rows of the tile.  The last round of down-projection tiles, when the
+// grid would run it mostly idle, is split along k (fp32 partials, reduced in
+// piece order by tail_reduce_kernel).
 // The weight tile is the MFMA A operand and the activation tile the B operand,
 // so each lane ends up holding 4 consecutive output columns of one row: the
 // epilogue stores 8 bytes per lane.  For GEMM-1 the weight tile holds 128
