@@ -232,13 +232,17 @@ def test_route_ties_and_signed_zero():
             assert np.abs(to_host(w) - ow).max() <= weight_tol(k, E)
 
 
-def test_permute_large_ids_direct():
-    """Permute on ids from brute-force-checkable random expert sets, E = 256."""
-    rng = np.random.default_rng(6)
-    T, E, k, H = 3000, 256, 5, 128
+# T * k up to 16 units of 1024 assignments runs the single-block permute, more
+# the count / scan / rank kernels: both sides of the boundary, E up to 256.
+@pytest.mark.parametrize("T,E,k", [(3000, 256, 5), (3277, 256, 5), (16384, 16, 1), (16385, 16, 1),
+                                   (20000, 8, 2)])
+def test_permute_direct(T, E, k):
+    """Permute on random distinct expert sets per token against the oracle, bit-exact."""
+    rng = np.random.default_rng(6 + T)
+    H = 128
     ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
     x = moegen.round_bf16(rng.standard_normal((T, H)).astype(np.float32))
-    log(f"[gpu] permute E=256 T={T} k={k}")
+    log(f"[gpu] permute E={E} T={T} k={k} ({(T * k + 1023) // 1024} units)")
     out = moe.moe_permute(to_dev(ids), to_dev(x), E)
     torch.cuda.synchronize()
     oc, oo, od, os_, oxp = oracle.permute(ids, x, E)
