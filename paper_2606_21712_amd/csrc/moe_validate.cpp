@@ -47,7 +47,7 @@ Check experts_topk(const char* fn, int32_t E, int32_t k) {
 Check tokens(const char* fn, int64_t T, int32_t k) {
   if (T < 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "T=%lld is negative", T);
   if (T > 0 && T > INT32_MAX / k)
-    return fail(MOE_ERR_INVALID_ARGUMENT, fn, "T*k=%lld exceeds INT32_MAX", T * (long long)k);
+    return fail(MOE_ERR_INVALID_ARGUMENT, fn, "T=%lld times k=%lld exceeds INT32_MAX", T, k);
   return Check{};
 }
 
