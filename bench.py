@@ -39,12 +39,19 @@ CPU_SAMPLE = {"tiny": 256, "mixtral4k": 4096, "mixtral32k_zipf": 4096, "deepseek
 
 
 def gemm_source_sha256() -> str:
+    """sha256 of the grouped-GEMM source (ffn.hip, then the common.h it includes)
+    with comments removed and whitespace collapsed, so that only code changes
+    invalidate counters taken on it."""
     import hashlib
+    import re
     csrc = os.path.join(ROOT, "paper_2606_21712_amd", "csrc")
     h = hashlib.sha256()
     for name in ("ffn.hip", "common.h"):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(csrc, name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)      # block comments
+        text = re.sub(r"//[^\n]*", " ", text)                    # line comments
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 
