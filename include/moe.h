@@ -107,7 +107,8 @@ moe_status moe_route(const float* logits, int64_t T, int32_t E, int32_t k, int32
  *   topk_ids, topk_weights      as moe_route
  *
  * Errors: as moe_route, plus INVALID_ARGUMENT for H not a positive multiple of
- * 64 and UNSUPPORTED for E > 64 (MOE_MAX_ROUTER_EXPERTS).
+ * 64 and UNSUPPORTED for E > 64 (MOE_MAX_ROUTER_EXPERTS) or a router matrix of
+ * 2 GiB or more.
  */
 moe_status moe_router_topk(const void* x, const void* w_router, int64_t T, int32_t E, int32_t k, int32_t H,
                            int32_t renormalize, float* logits, int32_t* topk_ids, float* topk_weights,

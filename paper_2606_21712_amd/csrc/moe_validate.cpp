@@ -133,6 +133,9 @@ Check validate_router_topk(const void* x, const void* w, int64_t T, int32_t E, i
     return fail(MOE_ERR_UNSUPPORTED, fn, "E=%lld exceeds %lld for the fused router", E, MOE_MAX_ROUTER_EXPERTS);
   MOE_TRY(tokens(fn, T, k));
   MOE_TRY(dim64(fn, "H", H));
+  // the router matrix is addressed with 32-bit byte offsets
+  if (int64_t(E) * int64_t(H) * 2 >= (int64_t(1) << 31))
+    return fail(MOE_ERR_UNSUPPORTED, fn, "E=%lld x H=%lld router matrix exceeds 2 GiB", E, H);
   if (renormalize != 0 && renormalize != 1)
     return fail(MOE_ERR_INVALID_ARGUMENT, fn, "renormalize=%lld must be 0 or 1", renormalize);
   if (T == 0) return Check{};

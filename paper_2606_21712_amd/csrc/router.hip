@@ -194,6 +194,208 @@ __global__ __launch_bounds__(64) void router_kernel(const uint16_t* __restrict__
   }
 }
 
+// Large batches: four wavefronts per block (64 tokens), the router matrix staged
+// through LDS in k-slices of 256 that the four share, so L2 serves it once per
+// block instead of once per wavefront.  Slices are double-buffered and filled by
+// direct global -> LDS loads; the 16-byte chunks of each 512-byte expert row are
+// stored at chunk ^ (row & 15), so the 16 expert rows an MFMA operand read
+// touches land on distinct banks.  Each wavefront streams its 16 token rows into
+// registers one slice ahead.  Selection as in router_kernel.
+constexpr int kLdsWaves = 4;
+constexpr int kSliceK = 256;                          // k per slice
+constexpr int kSliceRowBytes = kSliceK * 2;           // 512
+constexpr int kSliceSteps = kSliceK / 32;             // MFMA k-steps per slice
+
+template <int NB, int KMAX>
+__global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16_t* __restrict__ x,
+                                                                   const uint16_t* __restrict__ w, int64_t T,
+                                                                   int E, int k, int H, int renormalize,
+                                                                   float* __restrict__ logits_out,
+                                                                   int32_t* __restrict__ topk_ids,
+                                                                   float* __restrict__ topk_w) {
+  constexpr int EP = 16 * NB;
+  constexpr int V = EP / 4;
+  constexpr int kSliceBytes = EP * kSliceRowBytes;    // NB * 8 KB
+  __shared__ __attribute__((aligned(1024))) uint8_t ws0[kSliceBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t ws1[kSliceBytes];
+  __shared__ float s_log[kLdsWaves][kTok][EP + 1];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if (T < 0) {                                        // never taken: keeps the DMA-filled slices' reads
+    ws0[tid] = 0;
+    ws1[tid] = 0;
+  }
+  const int64_t t0 = (int64_t(blockIdx.x) * kLdsWaves + wave) * kTok;
+  const int r16 = lane & 15;
+  const int kq = lane >> 4;
+  const bool xv = t0 + r16 < T;
+  const bf16x8* xr = reinterpret_cast<const bf16x8*>(x + (xv ? t0 + r16 : 0) * H + kq * 8);
+  const bf16x8 zero = {};
+
+  // slice DMA: NB * 8 instructions of 1 KB (two 512-byte expert rows each), dealt
+  // over the four wavefronts; lane q fills row 2 i + q / 32, chunk position q % 32
+  const __amdgpu_buffer_rsrc_t rw =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w), 0, int(int64_t(E) * H * 2), 0x00020000);
+  constexpr int kDma = NB * 8;
+  constexpr int kDmaPerWave = (kDma + kLdsWaves - 1) / kLdsWaves;
+  // (a fixed-size array: sized by the template-dependent count, the host pass
+  // drops the kernel's launch stub)
+  static_assert(kDmaPerWave <= 8, "at most 64 experts");
+  uint32_t woff[8];
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int i = j * kLdsWaves + wave;               // instruction index
+    const int row = 2 * i + (lane >> 5);
+    const int pos = lane & 31;
+    const int chunk = pos ^ (row & 15);               // logical 16-byte chunk this lane fetches
+    woff[j] = row < E ? uint32_t(row) * uint32_t(H) * 2u + uint32_t(chunk) * 16u : 0x80000000u;
+  }
+  auto issue_w = [&](uint8_t* slice, int s) {
+    const int kb = s * kSliceRowBytes;
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) {
+      const int i = j * kLdsWaves + wave;
+      if (i < kDma) __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, slice + i * 1024, 16, woff[j], kb, 0, 0);
+    }
+  };
+  auto load_x = [&](bf16x8* a, int s) {
+#pragma unroll
+    for (int u = 0; u < kSliceSteps; ++u)
+      a[u] = xv ? __builtin_nontemporal_load(xr + (s * kSliceK + 32 * u) / 8) : zero;
+  };
+
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const uint8_t* slice, const bf16x8* a) {
+#pragma unroll
+    for (int u = 0; u < kSliceSteps; ++u) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int row = nb * 16 + r16;
+        const int chunk = 4 * u + kq;
+        const bf16x8 b = *reinterpret_cast<const bf16x8*>(slice + row * kSliceRowBytes + ((chunk ^ (row & 15)) * 16));
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u], b, acc[nb], 0, 0, 0);
+      }
+    }
+  };
+
+  const int S = H / kSliceK;
+  bf16x8 xa[2][kSliceSteps];
+  issue_w(ws0, 0);
+  load_x(xa[0], 0);
+  auto step = [&](uint8_t* cur, uint8_t* nxt, const bf16x8* a_cur, bf16x8* a_nxt, int s) {
+    __builtin_amdgcn_s_waitcnt(0x0F70);               // this slice's loads (and the x rows) landed
+    __syncthreads();                                  // ... for every wave; the other slice is free
+    if (s + 1 < S) {
+      issue_w(nxt, s + 1);
+      load_x(a_nxt, s + 1);
+    }
+    compute(cur, a_cur);
+  };
+  int s = 0;
+  for (; s + 2 <= S; s += 2) {
+    step(ws0, ws1, xa[0], xa[1], s);
+    step(ws1, ws0, xa[1], xa[0], s + 1);
+  }
+  if (s < S) step(ws0, ws1, xa[0], xa[1], s);
+
+  // 16 x 16 outputs: lane holds tokens 4 (lane / 16) + q of expert column lane % 16
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s_log[wave][4 * kq + q][nb * 16 + r16] = acc[nb][q];
+  __syncthreads();
+
+  // selection: 16 tokens per wavefront, token tt = lane / 4, lane g = lane % 4 holds
+  // experts g V .. g V + V - 1
+  const int tt = lane >> 2;
+  const int g = lane & 3;
+  const int64_t t = t0 + tt;
+  const bool valid = t < T;
+  const int e0 = g * V;
+  float vals[V];
+  uint32_t key[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const bool live = e0 + v < E;
+    vals[v] = live ? s_log[wave][tt][e0 + v] : 0.f;
+    key[v] = live ? orderable(vals[v]) : 0u;
+  }
+  if (logits_out != nullptr && valid) {
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if (e0 + v < E) logits_out[t * E + e0 + v] = vals[v];
+  }
+  uint32_t selk[KMAX];
+  uint32_t sele[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j < k) {
+      uint32_t m = key[0];
+#pragma unroll
+      for (int v = 1; v < V; ++v) m = max(m, key[v]);
+      m = quad_max(m);
+      uint32_t id = 0xFFFFFFFFu;
+#pragma unroll
+      for (int v = V - 1; v >= 0; --v) id = key[v] == m ? uint32_t(e0 + v) : id;
+      id = quad_min(id);
+#pragma unroll
+      for (int v = 0; v < V; ++v) key[v] = uint32_t(e0 + v) == id ? 0u : key[v];
+      selk[j] = m;
+      sele[j] = id;
+    } else {
+      selk[j] = 0u;
+      sele[j] = 0u;
+    }
+  }
+  const float lmax = from_orderable(selk[0]);
+  float p[KMAX];
+  float denom = 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j < k) {
+      p[j] = expf(from_orderable(selk[j]) - lmax);
+      denom += p[j];
+    }
+  }
+  if (!renormalize) {
+    float sum = 0.f;
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if (e0 + v < E) sum += expf(vals[v] - lmax);
+    denom = quad_sum(sum);
+  }
+  if (valid && g == 0) {
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        topk_ids[t * k + j] = int32_t(sele[j]);
+        topk_w[t * k + j] = p[j] / denom;
+      }
+    }
+  }
+}
+
+template <int NB>
+hipError_t launch_lds(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
+                      float* logits, int32_t* ids, float* wts, hipStream_t s) {
+  const dim3 grid(unsigned((T + kLdsWaves * kTok - 1) / (kLdsWaves * kTok)));
+  const dim3 block(kLdsWaves * 64);
+  if (k <= 4)
+    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, 4>), grid, block, s, x, w, T, E, k, H, renorm, logits, ids,
+               wts);
+  else if (k <= 8)
+    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, 8>), grid, block, s, x, w, T, E, k, H, renorm, logits, ids,
+               wts);
+  else
+    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, kMaxTopK>), grid, block, s, x, w, T, E, k, H, renorm, logits,
+               ids, wts);
+  return hipGetLastError();
+}
+
 template <int MB, int NB>
 hipError_t launch_mn(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
                      float* logits, int32_t* ids, float* wts, hipStream_t s) {
@@ -215,6 +417,9 @@ hipError_t launch_mn(const uint16_t* x, const uint16_t* w, int64_t T, int E, int
 template <int NB>
 hipError_t launch_nb(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
                      float* logits, int32_t* ids, float* wts, int num_cu, hipStream_t s) {
+  // Enough 64-token blocks for every compute unit: the LDS-staged kernel.
+  if (H % kSliceK == 0 && T >= int64_t(num_cu) * kLdsWaves * kTok)
+    return launch_lds<NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
   const int64_t waves_wanted = int64_t(num_cu) * 8;
   if (T >= waves_wanted * 64) return launch_mn<4, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
   if (T >= waves_wanted * 32) return launch_mn<2, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);

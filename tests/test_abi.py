@@ -210,6 +210,7 @@ def test_router_topk_validation(L):
     assert router(L, E=300) == UNSUPPORTED
     assert router(L, k=9) == INVALID
     assert router(L, H=96) == INVALID
+    assert router(L, E=64, k=2, H=1 << 24) == UNSUPPORTED             # 2 GiB router matrix
     assert router(L, renorm=3) == INVALID
     assert router(L, T=-1) == INVALID
     assert router(L, w=None) == INVALID

@@ -52,10 +52,15 @@ def check(x, w, k, renorm=1, exact_ties=False):
     return safe.mean()
 
 
-# T >= 65536 and >= 131072 give a wavefront 32 and 64 tokens (on 256 compute units)
+# With H % 256 != 0 (or fewer than 64 tokens per compute unit) the per-wavefront
+# kernel runs: T >= 65536 and >= 131072 give a wavefront 32 and 64 tokens (on 256
+# compute units).  H % 256 == 0 with T >= 16384 runs the LDS-staged kernel: 1 to 4
+# expert blocks, 4, 8 and 16 selection slots, ragged last block of 64 tokens.
 @pytest.mark.parametrize("T,E,k,H", [(1000, 8, 2, 256), (333, 64, 8, 448), (77, 3, 3, 64), (500, 40, 6, 4096),
                                      (129, 16, 4, 192), (257, 33, 16, 320), (5, 64, 1, 128),
-                                     (70001, 20, 3, 64), (140007, 64, 4, 128)])
+                                     (70001, 20, 3, 64), (140007, 64, 4, 128),
+                                     (16384, 8, 2, 768), (20000, 64, 8, 256), (17000, 40, 4, 512),
+                                     (33333, 20, 16, 1024)])
 def test_router_random(T, E, k, H):
     rng = np.random.default_rng(T + E + H)
     x = moegen.round_bf16(rng.standard_normal((T, H)).astype(np.float32))
