@@ -379,6 +379,164 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
   }
 }
 
+// Small batches (fewer than 8 sixteen-token wavefronts per compute unit): four
+// wavefronts per 16 tokens, each a quarter of the k range, their fp32 partial
+// logits added in wavefront order through LDS; wavefront 0 then selects.
+constexpr int kSplitWaves = 4;
+
+template <int NB, int KMAX>
+__global__ __launch_bounds__(kSplitWaves * 64) void router_splitk_kernel(const uint16_t* __restrict__ x,
+                                                                        const uint16_t* __restrict__ w, int64_t T,
+                                                                        int E, int k, int H, int renormalize,
+                                                                        float* __restrict__ logits_out,
+                                                                        int32_t* __restrict__ topk_ids,
+                                                                        float* __restrict__ topk_w) {
+  constexpr int EP = 16 * NB;
+  constexpr int V = EP / 4;
+  __shared__ float s_part[kSplitWaves][kTok][EP + 1];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  const int64_t t0 = int64_t(blockIdx.x) * kTok;
+  const int r16 = lane & 15;
+  const int kq = lane >> 4;
+  const int Hq = H / kSplitWaves;                     // a multiple of 32
+  const int kbase = wave * Hq;
+  const bool xv = t0 + r16 < T;
+  const bf16x8* xr = reinterpret_cast<const bf16x8*>(x + (xv ? t0 + r16 : 0) * H + kbase + kq * 8);
+  const bf16x8* wr[NB];
+  bool wv[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    wv[nb] = nb * 16 + r16 < E;
+    wr[nb] = reinterpret_cast<const bf16x8*>(w + int64_t(wv[nb] ? nb * 16 + r16 : 0) * H + kbase + kq * 8);
+  }
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16x8 zero = {};
+  int k0 = 0;
+  for (; k0 + 32 * kUnroll <= Hq; k0 += 32 * kUnroll) {
+    bf16x8 a[kUnroll], b[kUnroll][NB];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      a[u] = xv ? __builtin_nontemporal_load(xr + (k0 + 32 * u) / 8) : zero;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) b[u][nb] = wv[nb] ? wr[nb][(k0 + 32 * u) / 8] : zero;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u], b[u][nb], acc[nb], 0, 0, 0);
+  }
+  for (; k0 < Hq; k0 += 32) {
+    const bf16x8 a = xv ? __builtin_nontemporal_load(xr + k0 / 8) : zero;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 b = wv[nb] ? wr[nb][k0 / 8] : zero;
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[nb], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s_part[wave][4 * kq + q][nb * 16 + r16] = acc[nb][q];
+  __syncthreads();
+  if (wave != 0) return;
+
+  // selection: token tt = lane / 4, lane g = lane % 4 holds experts g V .. g V + V - 1
+  const int tt = lane >> 2;
+  const int g = lane & 3;
+  const int64_t t = t0 + tt;
+  const bool valid = t < T;
+  const int e0 = g * V;
+  float vals[V];
+  uint32_t key[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const bool live = e0 + v < E;
+    float l = 0.f;
+    if (live) {
+      l = s_part[0][tt][e0 + v];
+#pragma unroll
+      for (int q = 1; q < kSplitWaves; ++q) l += s_part[q][tt][e0 + v];   // quarters in k order
+    }
+    vals[v] = l;
+    key[v] = live ? orderable(l) : 0u;
+  }
+  if (logits_out != nullptr && valid) {
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if (e0 + v < E) logits_out[t * E + e0 + v] = vals[v];
+  }
+  uint32_t selk[KMAX];
+  uint32_t sele[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j < k) {
+      uint32_t m = key[0];
+#pragma unroll
+      for (int v = 1; v < V; ++v) m = max(m, key[v]);
+      m = quad_max(m);
+      uint32_t id = 0xFFFFFFFFu;
+#pragma unroll
+      for (int v = V - 1; v >= 0; --v) id = key[v] == m ? uint32_t(e0 + v) : id;
+      id = quad_min(id);
+#pragma unroll
+      for (int v = 0; v < V; ++v) key[v] = uint32_t(e0 + v) == id ? 0u : key[v];
+      selk[j] = m;
+      sele[j] = id;
+    } else {
+      selk[j] = 0u;
+      sele[j] = 0u;
+    }
+  }
+  const float lmax = from_orderable(selk[0]);
+  float p[KMAX];
+  float denom = 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j < k) {
+      p[j] = expf(from_orderable(selk[j]) - lmax);
+      denom += p[j];
+    }
+  }
+  if (!renormalize) {
+    float sum = 0.f;
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if (e0 + v < E) sum += expf(vals[v] - lmax);
+    denom = quad_sum(sum);
+  }
+  if (valid && g == 0) {
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        topk_ids[t * k + j] = int32_t(sele[j]);
+        topk_w[t * k + j] = p[j] / denom;
+      }
+    }
+  }
+}
+
+template <int NB>
+hipError_t launch_splitk(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
+                         float* logits, int32_t* ids, float* wts, hipStream_t s) {
+  const dim3 grid(unsigned((T + kTok - 1) / kTok));
+  const dim3 block(kSplitWaves * 64);
+  if (k <= 4)
+    MOE_LAUNCH("router_topk", (router_splitk_kernel<NB, 4>), grid, block, s, x, w, T, E, k, H, renorm, logits,
+               ids, wts);
+  else if (k <= 8)
+    MOE_LAUNCH("router_topk", (router_splitk_kernel<NB, 8>), grid, block, s, x, w, T, E, k, H, renorm, logits,
+               ids, wts);
+  else
+    MOE_LAUNCH("router_topk", (router_splitk_kernel<NB, kMaxTopK>), grid, block, s, x, w, T, E, k, H, renorm,
+               logits, ids, wts);
+  return hipGetLastError();
+}
+
 template <int NB>
 hipError_t launch_lds(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
                       float* logits, int32_t* ids, float* wts, hipStream_t s) {
@@ -421,6 +579,9 @@ hipError_t launch_nb(const uint16_t* x, const uint16_t* w, int64_t T, int E, int
   if (H % kSliceK == 0 && T >= int64_t(num_cu) * kLdsWaves * kTok)
     return launch_lds<NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
   const int64_t waves_wanted = int64_t(num_cu) * 8;
+  // Fewer than 8 sixteen-token wavefronts per compute unit: split k four ways.
+  if (H % (kSplitWaves * 32) == 0 && T < waves_wanted * kTok)
+    return launch_splitk<NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
   if (T >= waves_wanted * 64) return launch_mn<4, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
   if (T >= waves_wanted * 32) return launch_mn<2, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
   return launch_mn<1, NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
