@@ -37,6 +37,8 @@ CASES = {
     "k_eq_E": small("k_eq_E", T=260, H=64, E=4, k=4, F=64, seed=17),
     "T1": small("T1", T=1, H=64, E=8, k=2, F=64, seed=18),
     "H64_f32": small("H64_f32", T=333, H=64, E=5, k=2, F=64, seed=19, dtype="f32"),
+    # the largest expert count: most groups empty or a few rows
+    "e256_small": small("e256_small", T=300, H=128, E=256, k=8, F=192, seed=23),
     # few down-projection tiles and a long k (224 steps of 64)
     "longk_small": small("longk_small", T=1024, H=256, E=8, k=2, F=4096, seed=20),
 }
