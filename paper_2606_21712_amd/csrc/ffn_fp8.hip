@@ -247,16 +247,18 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
       }
       woff[i] = uint32_t(SWIGLU ? (r & 127) : r) * uint32_t(K) + cb;
     }
-    // gather: wave 1 loads the activation scales row by row (4 x 64 dwords): the
-    // byte offset of tile row 64 j + lane's token in step 0, or beyond the array
-    uint32_t stok[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int grow = row0 + 64 * j + lane;
-      stok[j] = (GATHER && wave == 1 && grow < row_stop) ? uint32_t(p.gather[grow]) * 4u : 0x80000000u;
+    // gather: waves 4-7 each load the activation scales of 64 tile rows, one dword
+    // per lane (spread over four waves, so no wave issues more than its operand
+    // loads plus one): the byte offset of tile row 64 (wave - 4) + lane's token in
+    // step 0, or beyond the array
+    uint32_t stok;
+    {
+      const int grow = row0 + 64 * (wave - 4) + lane;
+      stok = (GATHER && wave >= 4 && grow < row_stop) ? uint32_t(p.gather[grow]) * 4u : 0x80000000u;
     }
     // scale rows: wave 0 loads the weight tile's 256 scale dwords (GEMM-1: lanes
     // 0-31 the 128 gate rows, lanes 32-63 the up rows), wave 1 the activation tile's
+    // (without a gather: contiguous rows, one 16-byte load per lane)
     const uint32_t sw_lane = SWIGLU ? uint32_t((lane & 31) * 16) : uint32_t(lane * 16);
 
     auto issue = [&](uint8_t* stage, int kt) {
@@ -276,18 +278,14 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw1, stage + kWScaleOff, 16, voff, 0, 0, 0);
         else
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw0, stage + kWScaleOff, 16, voff, 0, 0, 0);
-      } else if (wave == 1) {
-        if (GATHER) {
-          const uint32_t step_off = uint32_t(int64_t(kt) * p.T * 4);
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff + 256 * j, 4,
-                                                     stok[j] == 0x80000000u ? stok[j] : stok[j] + step_off, 0,
-                                                     0, 0);
-        } else {
-          const uint32_t voff = uint32_t((int64_t(kt) * p.R + row0) * 4) + uint32_t(lane * 16);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff, 16, voff, 0, 0, 0);
-        }
+      }
+      if (GATHER && wave >= 4) {
+        const uint32_t step_off = uint32_t(int64_t(kt) * p.T * 4);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff + 256 * (wave - 4), 4,
+                                                 stok == 0x80000000u ? stok : stok + step_off, 0, 0, 0);
+      } else if (!GATHER && wave == 1) {
+        const uint32_t voff = uint32_t((int64_t(kt) * p.R + row0) * 4) + uint32_t(lane * 16);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, stage + kXScaleOff, 16, voff, 0, 0, 0);
       }
     };
 
