@@ -219,8 +219,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
       // GEMM-1: tile rows 0..127 are gate features n0.., rows 128..255 the same up features.
       woff[i] = uint32_t(SWIGLU ? (r & 127) : r) * uint32_t(rowb) + cb;
     }
-    // Activation passes whose 8 rows all lie past the tile are not issued.
-    auto issue = [&](uint8_t* stage, int kt) {
+    // The weight passes and the activation passes of a stage's loads.  Activation
+    // passes whose 8 rows all lie past the tile are not issued.
+    auto issue_w = [&](uint8_t* stage, int kt) {
       const int kb = kt * kRowBytes;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -228,6 +229,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
         __builtin_amdgcn_raw_ptr_buffer_load_lds((SWIGLU && i >= 2) ? rw1 : rw0, stage + blk * 1024, 16,
                                                  woff[i], kb, 0, 0);
       }
+    };
+    auto issue_a = [&](uint8_t* stage, int kt) {
+      const int kb = kt * kRowBytes;
 #pragma unroll
       for (int i = 0; i < 5; ++i) {
         const int blk = 8 * i + wave;
@@ -267,7 +271,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
           xf[mi] = *reinterpret_cast<const bf16x8*>(stage + kWOpBytes + row * kRowBytes + swz(row, c) * 16);
         }
       };
-      auto compute = [&](const uint8_t* stage) {
+      // MFMAs of a stage; the next stage's activation passes (ktn >= 0) are issued
+      // after the first sub-step's MFMAs.
+      auto compute = [&](const uint8_t* stage, uint8_t* nxt, int ktn) {
         if constexpr (NB > 0) {
           bf16x8 wf[2][2], xf[2][NB];
           frags(stage, 0, wf[0], xf[0]);
@@ -295,21 +301,32 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
             } else {
               __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
             }
+            if (s == 0 && ktn >= 0) {
+              __builtin_amdgcn_sched_barrier(0);
+              issue_a(nxt, ktn);
+              __builtin_amdgcn_sched_barrier(0);
+            }
           }
+        } else {
+          if (ktn >= 0) issue_a(nxt, ktn);
         }
       };
       // One k-step: wait for this stage's loads (own lanes, then all waves via the
-      // barrier, which also frees the other stage), start the next step's loads
-      // into the other stage, then run the MFMAs of this one.
+      // barrier, which also frees the other stage), then run the MFMAs of this one
+      // while the next step's loads go out into the other stage: the weight passes
+      // first, the activation passes after the first 16-k sub-step, so that the
+      // eight wavefronts' loads do not all queue at the texture unit at once and
+      // hold back the first MFMAs of the step.
       auto step = [&](uint8_t* cur, uint8_t* nxt, int kt) {
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
-        if (kt + 1 < kt1) issue(nxt, kt + 1);
-        compute(cur);
+        if (kt + 1 < kt1) issue_w(nxt, kt + 1);
+        compute(cur, nxt, kt + 1 < kt1 ? kt + 1 : -1);
       };
-      issue(st0, kt0);
+      issue_w(st0, kt0);
+      issue_a(st0, kt0);
       int kt = kt0;
       for (; kt + 2 <= kt1; kt += 2) {
         step(st0, st1, kt);
