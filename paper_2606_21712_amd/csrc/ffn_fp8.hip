@@ -261,14 +261,20 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
     // (without a gather: contiguous rows, one 16-byte load per lane)
     const uint32_t sw_lane = SWIGLU ? uint32_t((lane & 31) * 16) : uint32_t(lane * 16);
 
+    // A stage's loads: the activation codes first (gathered rows arrive last),
+    // then the weight codes, then the scales.
     auto issue = [&](uint8_t* stage, int kt) {
       const int kb = kt * kRowBytes;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int blk = 8 * i + wave;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int blk = 8 * i + wave;
         __builtin_amdgcn_raw_ptr_buffer_load_lds((SWIGLU && i >= 2) ? rw1 : rw0, stage + blk * 1024, 16,
                                                  woff[i], kb, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
       }
       // The scale rows' base goes into the per-lane offset, which the buffer range
       // check covers: rows past the end of a scale array read as zeros.
