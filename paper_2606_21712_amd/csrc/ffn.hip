@@ -277,6 +277,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
         if constexpr (NB > 0) {
           bf16x8 wf[2][2], xf[2][NB];
           frags(stage, 0, wf[0], xf[0]);
+          // Raised wave priority for the first two sub-steps: right after the
+          // barrier the other wavefront of the SIMD is issuing loads and fragment
+          // reads, and the MFMA stream should not wait behind them.
+          __builtin_amdgcn_s_setprio(1);
 #pragma unroll
           for (int s = 0; s < 4; ++s) {
             if (s < 3) frags(stage, s + 1, wf[(s + 1) & 1], xf[(s + 1) & 1]);
@@ -306,6 +310,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
               issue_a(nxt, ktn);
               __builtin_amdgcn_sched_barrier(0);
             }
+            if (s == 1) __builtin_amdgcn_s_setprio(0);
           }
         } else {
           if (ktn >= 0) issue_a(nxt, ktn);
