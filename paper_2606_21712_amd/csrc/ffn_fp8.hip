@@ -329,6 +329,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
       for (int ni = 0; ni < 2; ++ni) wf[0][ni] = frag(stage, wave_nrow<SWIGLU>(wn, ni) + rrow, 0);
 #pragma unroll
       for (int mi = 0; mi < 4; ++mi) xf[0][mi] = frag(stage + kOpBytes, wm * 128 + mi * 32 + rrow, 0);
+      // Raised wave priority for the first sub-step, while the other wavefront
+      // of the SIMD issues the step's loads.
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         if (s == 0) {
@@ -353,6 +356,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // one LDS read (12 for sub-step 1)
           }
           __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+          __builtin_amdgcn_s_setprio(0);
         } else {
           __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
         }
