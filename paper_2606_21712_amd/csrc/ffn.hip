@@ -32,7 +32,10 @@
 // (global_load_lds_dwordx4, no register staging), two stages deep, with the
 // 16-byte chunks of each 128-byte row XOR-swizzled so the MFMA operand reads
 // are free of bank conflicts; operand fragments are double-buffered in
-// registers so LDS latency hides behind the previous sub-step's MFMAs.
+// registers so LDS latency hides behind the previous sub-step's MFMAs.  After
+// each step's barrier a wavefront issues the next stage's weight loads, then
+// (at raised wave priority) the first sub-step's MFMAs, then the activation
+// loads, so the texture unit is not flooded while the MFMA stream restarts.
 #include <algorithm>
 #include <type_traits>
 
