@@ -94,6 +94,24 @@ CASES = {
     "f8_uniform": moegen.MoEConfig("f8_uniform", T=300, H=128, E=8, k=3, F=256, seed=34, routing="uniform"),
 }
 
+
+def _random_cases(n=4, seed=2027):
+    """Seeded random shapes within the MXFP8 limits (H, F multiples of 128)."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    for i in range(n):
+        E = int(rng.choice([1, 3, 5, 8, 16, 64]))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        T = int(rng.integers(1, 1500))
+        H = 128 * int(rng.integers(1, 6))
+        F = 128 * int(rng.integers(1, 5))
+        Fs = int(rng.choice([0, 256]))
+        out[f"f8_rand{i}"] = moegen.MoEConfig(f"f8_rand{i}", T=T, H=H, E=E, k=k, F=F, Fs=Fs, seed=40 + i)
+    return out
+
+
+CASES.update(_random_cases())
+
 # Accumulation error of the block-scaled fp8 MFMA, as a fraction of sum_k |a_k b_k|:
 # measured on gfx950 at 1.26e-4 for K = 512 random E4M3 codes over their whole
 # range with random scales (far coarser than fp32's 6e-8 per addition: the matrix
