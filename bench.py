@@ -3,16 +3,25 @@
 
 One step = the whole layer (route -> permute -> grouped SwiGLU FFN [-> shared
 expert] -> combine) over one synthetic expert batch whose inputs are already
-resident in HBM.  The default workload is the Mixtral-shaped layer: 4096
-tokens, hidden 4096, 8 experts, top-2, FFN dim 14336, bf16, near-uniform
-routing.  Prints ONE JSON line on stdout; progress goes to stderr.
+resident in HBM.  The default workload is the large memory-constrained expert
+batch: 131072 tokens, hidden 4096, 64 experts, top-4, FFN dim 4096, bf16, with
+lognormal expert loads whose three smallest experts hold 1, 17 and 31 rows.
+Prints ONE JSON line on stdout; progress goes to stderr.
 
 Per-kernel durations come from the library's own HIP-event profiler, recorded
 on the launch stream inside the timed region.  The roofline figure is for the
 dominant kernel, GEMM-1 (gate/up projections + SwiGLU): algorithmic flops
 4*H*F*R per launch over its average launch duration, against the 2.5 PFLOP/s
-dense bf16 MFMA peak.  The CPU baseline times the fp64 oracle on a bounded
-sample of tokens of the same workload on the host cores.
+dense bf16 MFMA peak.  Route, permute and combine are then timed call by call,
+cold (a 1 GiB buffer read and written before each call, flushing L2 and the
+256 MB Infinity Cache) and warm, as median / min / max over repetitions.  The
+CPU baseline times the fp64 oracle on a bounded sample of tokens of the same
+workload on the host cores.
+
+Other modes: --profile-run (a short run for rocprofv3 counter passes),
+--summarize DIR (tables from rocprofv3 output: kernel times, MFMA busy, clock,
+HBM bytes against the algorithmic bytes), --sweep (expert-batch sweep with a
+fitted runtime model), --mxfp8, --route-probe, --router-probe.
 """
 from __future__ import annotations
 
@@ -56,21 +65,25 @@ def gemm_source_sha256() -> str:
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per GEMM-1 launch from the committed counter summary, or None when
-    the summary is for another workload or the grouped-GEMM source changed since
-    (the hash covers ffn.hip followed by the common.h it includes)."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", f"ffn_gemm1_gate_up_{workload}_hbm_traffic.md")
-    if not os.path.exists(path):
-        return None
-    fields = {}
-    for line in open(path):
-        if ":" in line and line.split(":")[0] in ("source_sha256", "gemm1_traffic_bytes_per_launch"):
-            k, v = line.split(":", 1)
-            fields[k.strip()] = v.strip()
-    if fields.get("source_sha256") != gemm_source_sha256():
-        return None
-    return float(fields["gemm1_traffic_bytes_per_launch"])
+    """L2-egress bytes (FETCH_SIZE + WRITE_SIZE, calibrated) per GEMM-1 launch from the
+    committed rocprofv3 summary of the workload, or None when there is none or the
+    grouped-GEMM source changed since the counters were taken (the hash covers
+    ffn.hip followed by the common.h it includes)."""
+    for name in (f"moe_layer_{workload}_rocprof.md", f"ffn_gemm1_gate_up_{workload}_hbm_traffic.md"):
+        path = os.path.join(ROOT, "profiles", name)
+        if not os.path.exists(path):
+            continue
+        fields = {}
+        for line in open(path):
+            if ":" in line and line.split(":")[0] in ("source_sha256", "gemm1_traffic_bytes_per_launch"):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+        if "gemm1_traffic_bytes_per_launch" not in fields:
+            continue
+        if fields.get("source_sha256") != gemm_source_sha256():
+            return None
+        return float(fields["gemm1_traffic_bytes_per_launch"])
+    return None
 
 
 GEMM1 = "ffn_gemm1_gate_up"
@@ -390,17 +403,280 @@ def expert_batch_sweep(shape: str, steps: int, warmup: int):
                       "saturation_tokens_per_expert": sat * cfg.k / cfg.E}), flush=True)
 
 
+# --------------------------------------------------------------------------- algorithmic work per kernel
+def algorithmic_work(c, role: str, gather: bool = True):
+    """(flops, bytes) one launch of a kernel of the layer must do at the least on
+    workload c: every operand read once, every result written once, no padding.
+    role is a kernel label from kernel_label() (".shared" for the shared expert)."""
+    b = 4 if c.dtype == "f32" else 2
+    T, H, E, k, F, Fs, R = c.T, c.H, c.E, c.k, c.F, c.Fs, c.R
+    units = (R + 1023) // 1024
+    shared = role.endswith(".shared")
+    base = role.split(".")[0]
+    if base == "route":
+        return 0.0, T * E * 4 + T * k * 8
+    if base == "permute_count":
+        return 0.0, R * 4 + units * E * 4
+    if base == "permute_scan":
+        return 0.0, 2 * units * E * 4 + E * 4
+    if base == "permute_rank":
+        return 0.0, R * 4 + units * E * 4 + E * 4 + (E + 1) * 4 + 2 * R * 4
+    if base in ("permute_small", "permute_maps"):
+        return 0.0, R * 4 + E * 4 + (E + 1) * 4 + 2 * R * 4
+    if base == "permute_copy":
+        return 0.0, T * H * b + R * H * b + R * 4
+    if base == "combine":
+        return 0.0, R * H * b + T * H * b * (2 if Fs else 1) + T * k * 8
+    if base == "gemm1":
+        if shared:
+            return 4.0 * H * Fs * T, 2 * Fs * H * b + T * H * b + T * Fs * b
+        rows_in = T * H * b + R * 4 if gather else R * H * b
+        return 4.0 * H * F * R, 2 * E * F * H * b + rows_in + R * F * b
+    if base == "gemm2":
+        if shared:
+            return 2.0 * H * Fs * T, Fs * H * b + T * Fs * b + T * H * b
+        return 2.0 * H * F * R, E * H * F * b + R * F * b + R * H * b
+    return 0.0, 0
+
+
+def kernel_label(name: str) -> str:
+    """Short label of a kernel from its demangled name (rocprofv3 traces)."""
+    import re
+    m = re.search(r"(\w+)_kernel(<[^()]*>)?\(", name)
+    if not m:
+        return name.split("(")[0].strip()
+    base, tmpl = m.group(1), m.group(2) or ""
+    if base == "grouped_gemm_bf16" or base == "grouped_gemm_f32" or base == "grouped_gemm_fp8":
+        return "gemm1" if tmpl.startswith("<true") else "gemm2"
+    return base
+
+
+# --------------------------------------------------------------------------- cold / warm timing
+def time_calls(calls, stream, reps: int = 20):
+    """Median / min / max duration of each call, cold and warm.  calls = [(name, fn,
+    algorithmic bytes)].  Cold: a 1 GiB buffer is read and written (on the same
+    stream) right before each timed call, which evicts the call's operands from the
+    L2s and the 256 MB Infinity Cache; warm: the call runs again right after
+    itself.  HIP events on the launch stream bracket each call."""
+    import torch
+    scratch = torch.zeros(1 << 28, dtype=torch.float32, device="cuda")     # 1 GiB
+    out = {}
+    for name, fn, nbytes in calls:
+        res = {}
+        for mode in ("cold", "warm"):
+            fn()
+            ts = []
+            for _ in range(reps):
+                if mode == "cold":
+                    scratch.add_(1.0)
+                ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ev0.record(stream)
+                fn()
+                ev1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(ev0.elapsed_time(ev1) * 1e3)
+            med = float(np.median(ts))
+            gbs = nbytes / (med * 1e-6) / 1e9
+            res[mode] = dict(median_us=round(med, 2), min_us=round(float(np.min(ts)), 2),
+                             max_us=round(float(np.max(ts)), 2), GBps=round(gbs, 1),
+                             frac_hbm=round(gbs / PEAK_HBM_GBS, 4))
+        out[name] = dict(bytes=int(nbytes), reps=reps, **res)
+    del scratch
+    return out
+
+
+# --------------------------------------------------------------------------- rocprofv3 summaries
+# What the profile passes collect (one rocprofv3 --pmc run each; a run may hold at
+# most 8 SQ, 4 TCC, 2 GRBM counters).
+PMC_PASSES = {
+    "sq": "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_WAVE_CYCLES "
+          "SQ_WAIT_ANY SQ_WAIT_INST_LDS SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE",
+    "fetch": "FETCH_SIZE GRBM_GUI_ACTIVE",
+    "write": "WRITE_SIZE GRBM_GUI_ACTIVE",
+}
+NUM_XCD, NUM_CU, NUM_SIMD = 8, 256, 1024
+BF16_FLOP_PER_CU_CLK = 4096           # dense bf16 MFMA, gfx950
+
+
+def _read_csv(path):
+    import csv
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _segments(dispatches):
+    """Split (dispatch_id, label, ...) records, ordered by dispatch id, into layer
+    steps: a step starts at each route launch.  Within a step the second GEMM-1 or
+    GEMM-2 launch is the shared expert's.  Returns [(step_index, label, record)]."""
+    out, step, seen = [], -1, {}
+    for rec in dispatches:
+        lab = rec["label"]
+        if lab == "route":
+            step += 1
+            seen = {}
+        if lab in ("gemm1", "gemm2"):
+            n = seen.get(lab, 0)
+            seen[lab] = n + 1
+            if n == 1:
+                lab = lab + ".shared"
+        out.append((step, lab, rec))
+    return out
+
+
+def summarize(root, c, warmup: int, steps: int, gather: bool = True):
+    """Markdown tables from the rocprofv3 output under root:
+    root/trace/*kernel_trace.csv (a default bench.py run: warmup, then the timed
+    steps), root/<pass>/*counter_collection.csv (--profile-run under --pmc), and
+    root/copy_<pass>/*counter_collection.csv (--copy-calibration BYTES under --pmc;
+    the copy's size is read from root/copy_bytes.txt)."""
+    import glob
+    known = ("route", "permute_count", "permute_scan", "permute_rank", "permute_small", "permute_maps",
+             "permute_copy", "tile_prefix", "gemm1", "gemm2", "tail_reduce", "combine")
+
+    lines = [f"Workload {c.name}: T={c.T} H={c.H} E={c.E} k={c.k} F={c.F} Fs={c.Fs} {c.dtype}, "
+             f"{'gather' if gather else 'x_perm'} path.", ""]
+    # ---------------------------------------------------------------- kernel trace
+    traced = {}
+    for path in sorted(glob.glob(os.path.join(root, "trace", "*kernel_trace.csv"))):
+        rows = []
+        for r in _read_csv(path):
+            lab = kernel_label(r["Kernel_Name"])
+            if lab in known:
+                rows.append(dict(id=int(r["Dispatch_Id"]), label=lab, name=r["Kernel_Name"],
+                                 us=(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+        rows.sort(key=lambda r: r["id"])
+        for st, lab, rec in _segments(rows):
+            if warmup <= st < warmup + steps:
+                traced.setdefault(lab, []).append(rec["us"])
+    if traced:
+        step_us = sum(float(np.mean(v)) * len(v) / steps for v in traced.values())
+        lines += [f"Kernel trace (rocprofv3 --kernel-trace), the {steps} timed steps after {warmup} warmup "
+                  "steps:", "",
+                  "| kernel | launches | avg us | median us | min us | max us | % of step |",
+                  "|---|---|---|---|---|---|---|"]
+        for lab, v in sorted(traced.items(), key=lambda kv: -sum(kv[1])):
+            lines.append(f"| {lab} | {len(v)} | {np.mean(v):.2f} | {np.median(v):.2f} | {np.min(v):.2f} | "
+                         f"{np.max(v):.2f} | {100 * np.mean(v) * len(v) / steps / step_us:.2f} |")
+        lines += ["", f"Sum of kernel averages per step: {step_us / 1e3:.3f} ms -> "
+                      f"{c.T / (step_us * 1e-6) / 1e6:.3f} M tokens/s.", ""]
+    bench_json = os.path.join(root, "trace", "bench.json")
+    if os.path.exists(bench_json):
+        line = [ln for ln in open(bench_json) if ln.startswith("{")][-1]
+        bj = json.loads(line)
+        lines += [f"The same run's bench.py line: {bj['ms_per_step']} ms/step, {bj['value']:.0f} tokens/s; "
+                  f"its GEMM-1 (HIP events in the timed region) {bj['kernels_us'].get(GEMM1)} us, "
+                  f"roofline.frac {bj['roofline']['frac']}.", ""]
+    # ---------------------------------------------------------------- counters
+    calib = {}
+    copy_bytes_path = os.path.join(root, "copy_bytes.txt")
+    copy_bytes = int(open(copy_bytes_path).read().split()[0]) if os.path.exists(copy_bytes_path) else None
+    per = {}                       # label -> counter -> [values]; label -> "us" -> [durations]
+    for path in sorted(glob.glob(os.path.join(root, "*", "*counter_collection.csv"))):
+        pass_name = os.path.basename(os.path.dirname(path))
+        by_disp = {}
+        for r in _read_csv(path):
+            d = by_disp.setdefault(int(r["Dispatch_Id"]), dict(id=int(r["Dispatch_Id"]), name=r["Kernel_Name"],
+                                                              label=kernel_label(r["Kernel_Name"]),
+                                                              counters={}))
+            d["counters"][r["Counter_Name"]] = float(r["Counter_Value"])
+            d["us"] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        recs = sorted(by_disp.values(), key=lambda d: d["id"])
+        if pass_name.startswith("copy_"):
+            for d in recs:
+                if "copy" in d["name"].lower():
+                    for k, v in d["counters"].items():
+                        calib.setdefault(k, []).append(v)
+            continue
+        for st, lab, d in _segments([r for r in recs if r["label"] in known]):
+            if st < 1:
+                continue                          # the profile run's first step warms up
+            slot = per.setdefault(lab, {})
+            for k, v in d["counters"].items():
+                slot.setdefault(k, []).append(v)
+            slot.setdefault("us", []).append(d["us"])
+    factor = {}
+    for k in ("FETCH_SIZE", "WRITE_SIZE"):
+        if copy_bytes and calib.get(k):
+            factor[k] = copy_bytes / (float(np.median(calib[k])) * 1024.0)
+    if per:
+        lines += ["Counters (rocprofv3 --pmc, one pass per counter set, dispatches serialized by the "
+                  "profiler; averages over the profile run's layer steps 2-3, plus its x_perm permute):", ""]
+        if factor:
+            lines += [f"HBM-byte calibration: a plain {copy_bytes / 2**30:.2f} GiB device copy reads "
+                      f"FETCH_SIZE x {factor.get('FETCH_SIZE', float('nan')):.3f} and WRITE_SIZE x "
+                      f"{factor.get('WRITE_SIZE', float('nan')):.3f} of its size; the same factors scale the "
+                      "kernels' counters below.", ""]
+        lines += ["Columns: duration under the counter passes; shader clock = GRBM_GUI_ACTIVE per XCD / "
+                  "duration (kernels of 100 us or more); MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x "
+                  "1024 SIMDs); MFMA-work cycles = counted bf16 flop (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) / "
+                  "(256 CUs x 4096 flop per cycle), over the elapsed cycles; waiting = SQ_WAIT_ANY / "
+                  "SQ_WAVE_CYCLES, LDS-issue wait = SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES; bytes = FETCH_SIZE + "
+                  "WRITE_SIZE (bytes leaving or entering the L2s: Infinity Cache hits included), calibrated; "
+                  "GB/s = algorithmic bytes / the traced average duration (* : kernel not in the timed "
+                  "steps, duration of the counter pass).", "",
+                  "| kernel | us (pmc run) | clock GHz | MFMA busy % | MFMA-work cycles / elapsed | "
+                  "counted bf16 flop / algorithmic | wave-cycles waiting % | LDS-issue wait % | "
+                  "L2-egress bytes | / algorithmic bytes | algorithmic GB/s | % of 8 TB/s |",
+                  "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+        for lab in sorted(per, key=lambda l: -float(np.mean(per[l]["us"]))):
+            s = per[lab]
+            m = {k: float(np.mean(v)) for k, v in s.items()}
+            us = m["us"]
+            grbm = m.get("GRBM_GUI_ACTIVE")
+            cyc = grbm / NUM_XCD if grbm else None               # elapsed cycles (per XCD)
+            # the GRBM window includes the dispatch itself, so the clock is meaningful
+            # for long kernels only
+            clk = cyc / (us * 1e3) if cyc and us >= 100 else None
+            busy = 100 * m["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * NUM_SIMD) \
+                if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in m else None
+            flops, nbytes = algorithmic_work(c, lab, gather)
+            cflop = m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
+            work = cflop / (NUM_CU * BF16_FLOP_PER_CU_CLK) / cyc if cyc and cflop else None
+            wait = 100 * m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"] \
+                if m.get("SQ_WAVE_CYCLES") and "SQ_WAIT_ANY" in m else None
+            lwait = 100 * m["SQ_WAIT_INST_LDS"] / m["SQ_WAVE_CYCLES"] \
+                if m.get("SQ_WAVE_CYCLES") and "SQ_WAIT_INST_LDS" in m else None
+            hbm = None
+            if "FETCH_SIZE" in m and "WRITE_SIZE" in m and factor:
+                hbm = m["FETCH_SIZE"] * 1024 * factor["FETCH_SIZE"] + m["WRITE_SIZE"] * 1024 * factor["WRITE_SIZE"]
+            t_us = float(np.mean(traced[lab])) if lab in traced else None
+            mark = "" if t_us else " *"
+            gbs = nbytes / ((t_us or us) * 1e3) if nbytes else None
+
+            def f(v, fmt):
+                return "-" if v is None else format(v, fmt)
+            lines.append(f"| {lab} | {f(us, '.1f')} | {f(clk, '.3f')} | {f(busy, '.1f')} | {f(work, '.3f')} | "
+                         f"{f(cflop / flops if flops and cflop else None, '.4f')} | {f(wait, '.1f')} | "
+                         f"{f(lwait, '.1f')} | {f(hbm / 1e6 if hbm else None, '.1f')} MB | "
+                         f"{f(hbm / nbytes if hbm and nbytes else None, '.2f')} | {f(gbs, '.0f')}{mark} | "
+                         f"{f(100 * gbs / PEAK_HBM_GBS if gbs else None, '.1f')}{mark} |")
+        lines.append("")
+        g = per.get("gemm1")
+        if g and "FETCH_SIZE" in g and "WRITE_SIZE" in g and factor:
+            hbm = float(np.mean(g["FETCH_SIZE"])) * 1024 * factor["FETCH_SIZE"] + \
+                float(np.mean(g["WRITE_SIZE"])) * 1024 * factor["WRITE_SIZE"]
+            lines += [f"source_sha256: {gemm_source_sha256()}", f"gemm1_traffic_bytes_per_launch: {hbm:.6g}", ""]
+    print("\n".join(lines))
+
+
 def main():
     import moegen
 
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[1])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="mixtral4k", choices=sorted(moegen.CONFIGS))
+    ap.add_argument("--config", default="memconstrained", choices=sorted(moegen.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather", action="store_true",
                     help="materialize x_perm in moe_permute instead of gathering rows in the grouped FFN")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="a short run for rocprofv3 counter passes: 1 warmup and 2 layer steps, then one "
+                         "moe_permute that also writes x_perm; no profiler pass, no cold/warm timing, no "
+                         "CPU baseline")
+    ap.add_argument("--summarize", metavar="DIR", default=None,
+                    help="print markdown tables from the rocprofv3 output under DIR (kernel traces and "
+                         "counter passes of --profile-run / default runs of --config)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
     ap.add_argument("--sweep", choices=["mixtral", "deepseek", "memconstrained"], default=None,
@@ -412,6 +688,9 @@ def main():
     ap.add_argument("--route-probe", action="store_true",
                     help="only time moe_route at 2^20 tokens (bandwidth probe), cold and warm")
     args = ap.parse_args()
+    if args.summarize:
+        return summarize(args.summarize, moegen.CONFIGS[args.config], args.warmup, args.steps,
+                         gather=not args.no_gather)
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
     if args.route_probe:
@@ -449,11 +728,28 @@ def main():
     wg, wu, wd = to_dev(I.w_gate, torch), to_dev(I.w_up, torch), to_dev(I.w_down, torch)
     shared = (to_dev(I.ws_gate, torch), to_dev(I.ws_up, torch), to_dev(I.ws_down, torch)) if c.Fs \
         else (None, None, None)
-    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt, gather=not args.no_gather)
+    gather = not args.no_gather
+    layer = moe.MoELayer(c.T, c.H, c.E, c.k, c.F, c.Fs, dtype=dt, gather=gather)
     stream = torch.cuda.current_stream()
 
     def step():
         layer.run(x, logits, wg, wu, wd, *shared, renormalize=c.renormalize, stream=stream)
+
+    if args.profile_run:
+        # what the counter passes see: one warmup step, two steps, then one permute
+        # that writes x_perm (the copy-path kernel), each dispatch serialized by the
+        # profiler
+        for i in range(3):
+            log(f"profile run: layer step {i + 1} of 3")
+            step()
+            torch.cuda.synchronize()
+        xp = torch.empty((c.R, c.H), dtype=dt, device="cuda")
+        out = dict(layer.perm, x_perm=xp)
+        moe.moe_permute(layer.topk_ids, x, c.E, out=out, ws=layer.ws_perm, stream=stream)
+        torch.cuda.synchronize()
+        log("profile run: done")
+        print(json.dumps({"profile_run": c.name, "steps": 3}), flush=True)
+        return
 
     for _ in range(args.warmup):
         step()
@@ -493,23 +789,33 @@ def main():
     achieved = gemm1_flops / (g1 * 1e-6) / 1e12 if g1 else None
     ffn_tflops = c.flops() / (ffn_us * 1e-6) / 1e12 if ffn_us else None
 
+    # Route, permute and combine call by call, cold and warm.  The buffers hold the
+    # last step's intermediates, so each call sees the layer's own inputs.
+    log("timing route / permute / combine call by call, cold and warm")
     b = 4 if c.dtype == "f32" else 2
-    bytes_alg = {
-        "route": c.T * c.E * 4 + c.T * c.k * 8,
-        # ids read + dest_rows and sorted_token_ids written (+ x read and x_perm written
-        # when the rows are materialized rather than gathered by the grouped FFN)
-        "permute": 3 * R * 4 + (0 if not args.no_gather else c.T * c.H * b + R * c.H * b),
-        "combine": R * c.H * b + c.T * c.H * b * (2 if c.Fs else 1) + c.T * c.k * 8,
-    }
-    perm_us = sum(kernels[k]["avg_us"] for k in kernels if k.startswith("permute_"))
-    copy_gbs = stream_copy_gbps()
-    bw = {"stream_copy_GBps": round(copy_gbs, 1)}
-    for name, us in (("route", kernels.get("route", {}).get("avg_us")), ("permute", perm_us),
-                     ("combine", kernels.get("combine", {}).get("avg_us"))):
-        if us:
-            gbs = bytes_alg[name] / (us * 1e-6) / 1e9
-            bw[name] = dict(us=round(us, 2), GBps=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 3),
-                            frac_copy=round(gbs / copy_gbs, 3))
+    maps_bytes = R * 4 + 2 * R * 4 + c.E * 4 + (c.E + 1) * 4
+    xp = torch.empty((R, c.H), dtype=dt, device="cuda")
+    perm_copy = dict(layer.perm, x_perm=xp)
+    perm_maps = dict(layer.perm, x_perm=None)
+    calls = [
+        ("route", lambda: moe.moe_route(logits, c.k, c.renormalize, layer.topk_ids, layer.topk_weights,
+                                        stream=stream),
+         c.T * c.E * 4 + c.T * c.k * 8),
+        ("permute_maps", lambda: moe.moe_permute(layer.topk_ids, x, c.E, out=perm_maps, ws=layer.ws_perm,
+                                                 stream=stream),
+         maps_bytes),
+        ("permute_with_x_perm", lambda: moe.moe_permute(layer.topk_ids, x, c.E, out=perm_copy, ws=layer.ws_perm,
+                                                        stream=stream),
+         maps_bytes + c.T * c.H * b + R * c.H * b),
+        ("combine", lambda: moe.moe_combine(layer.y_perm, layer.perm["dest_rows"], layer.topk_weights,
+                                            layer.y_shared, y=layer.y, stream=stream),
+         R * c.H * b + c.T * c.H * b * (2 if c.Fs else 1) + c.T * c.k * 8),
+    ]
+    bw = time_calls(calls, stream)
+    del xp, perm_copy
+    step()                                               # leave y as the layer's output
+    torch.cuda.synchronize()
+    bw["stream_copy_GBps"] = round(stream_copy_gbps(), 1)
 
     out = {
         "metric": METRIC,
@@ -526,7 +832,7 @@ def main():
         "data": "synthetic (seeded generator; random-init expert weights)",
         "config": {"workload": c.name, "tokens": c.T, "hidden": c.H, "experts": c.E, "top_k": c.k,
                    "ffn_dim": c.F, "shared_ffn_dim": c.Fs, "routing": c.routing, "seed": c.seed,
-                   "path": "permute maps + gather-fused grouped FFN" if not args.no_gather
+                   "path": "permute maps + gather-fused grouped FFN" if gather
                    else "permute with x_perm + grouped FFN"},
         "ffn_tflops": round(ffn_tflops, 1) if ffn_tflops else None,
         "ffn_frac_peak": round(ffn_tflops / peak, 4) if ffn_tflops else None,
