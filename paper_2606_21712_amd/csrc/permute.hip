@@ -2,17 +2,20 @@
 // expert, then a row gather of x into expert-grouped order, on gfx950.
 //
 // The assignment list (token-major, a = t*k + j) is cut into units of 1024
-// consecutive assignments, one wavefront each.  Within a wavefront, the lanes
-// holding the same expert find each other with 8 ballots over the id bits (a
-// match mask); a lane's rank among equal experts is the popcount of the match
-// mask below it, so the order inside an expert group is the assignment order,
-// i.e. ascending token.  Four kernels, no atomics (batches of at most 16 units
-// run the first three as one single-block kernel):
-//   count : per-unit, per-expert counts                      -> uc[E][units]
-//   scan  : per expert, exclusive scan over units; totals    -> uc, counts
-//   rank  : offsets = exclusive scan of counts; every assignment's row
-//           = offsets[e] + uc[e][unit] + running count + rank -> dest_rows, sorted_token_ids
+// consecutive assignments, one wavefront each, which loads its unit's ids (16
+// per lane) up front.  Within a wavefront, the lanes holding the same expert
+// find each other with log2(E) ballots over the id bits (a match mask); a
+// lane's rank among equal experts is the popcount of the match mask below it,
+// so the order inside an expert group is the assignment order, i.e. ascending
+// token.  No atomics.  Launches:
+//   count : per block of 4 units, per-expert totals               -> bc[E][blocks]
+//   rank  : per expert, the totals of the blocks before this one and of all
+//           blocks (read from bc: scan and rank fused); offsets = exclusive
+//           scan of the totals; every assignment's row = offsets[e] + earlier
+//           blocks' and units' counts + rank                     -> counts, offsets,
+//                                                                   dest_rows, sorted_token_ids
 //   copy  : one wavefront per token reads x[t] once and writes its k rows.
+// Batches of at most 16 units run count and rank as one single-block kernel.
 #include "common.h"
 #include "moe_internal.h"
 
@@ -35,76 +38,149 @@ __device__ __forceinline__ uint64_t wave_match(int id, bool valid, int nbits) {
   return m;
 }
 
-__global__ __launch_bounds__(kThreads) void permute_count_kernel(const int32_t* __restrict__ ids,
-                                                                int64_t R, int E, int nbits,
-                                                                int64_t Upad,
-                                                                int32_t* __restrict__ uc) {
-  __shared__ int32_t cnt[kWavesPerBlock][kMaxExperts];
-  const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x / kWave;
-  for (int e = lane; e < E; e += kWave) cnt[w][e] = 0;
-  __syncthreads();
-  const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + w;
-  const int64_t base = unit * kUnit;
-  const uint64_t below = (1ull << lane) - 1ull;
+// The unit's kIters ids of this lane, all loads issued before any is used (-1
+// past the end).  Lane l holds assignments base + 64 it + l.
+__device__ __forceinline__ void load_unit_ids(const int32_t* __restrict__ ids, int64_t base, int64_t R,
+                                              int lane, int (&idv)[kIters]) {
+#pragma unroll
   for (int it = 0; it < kIters; ++it) {
     const int64_t a = base + it * kWave + lane;
-    const bool valid = a < R;
-    const int id = valid ? ids[a] : 0;
+    idv[it] = a < R ? __builtin_nontemporal_load(ids + a) : -1;
+  }
+}
+
+// Per-expert counts of one unit into cnt (zeroed by the caller): the lanes of a
+// match group add their size once, through the group's lowest lane.
+__device__ __forceinline__ void count_unit(const int (&idv)[kIters], int nbits, int lane,
+                                           int32_t* __restrict__ cnt) {
+  const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int it = 0; it < kIters; ++it) {
+    const bool valid = idv[it] >= 0;
+    const int id = valid ? idv[it] : 0;
     const uint64_t match = wave_match(id, valid, nbits);
-    if (valid && (match & below) == 0ull) cnt[w][id] += __popcll(match);   // one leader per expert
+    if (valid && (match & below) == 0ull) cnt[id] += __popcll(match);
   }
-  __syncthreads();
-  for (int e = lane; e < E; e += kWave) uc[int64_t(e) * Upad + unit] = cnt[w][e];
 }
 
-__global__ __launch_bounds__(kThreads) void permute_scan_kernel(int32_t* __restrict__ uc, int64_t U,
-                                                               int64_t Upad,
-                                                               int32_t* __restrict__ counts) {
-  const int e = blockIdx.x;
-  int32_t* row = uc + int64_t(e) * Upad;
-  const int64_t per = (U + kThreads - 1) / kThreads;
-  const int64_t lo = int64_t(threadIdx.x) * per;
-  const int64_t hi = lo + per < U ? lo + per : U;
-  int32_t s = 0;
-  for (int64_t u = lo; u < hi; ++u) s += row[u];
-  int32_t total;
-  int32_t run = block_exclusive_scan256(s, &total);
-  for (int64_t u = lo; u < hi; ++u) {
-    const int32_t c = row[u];
-    row[u] = run;
-    run += c;
-  }
-  if (threadIdx.x == 0) counts[e] = total;
-}
-
-__global__ __launch_bounds__(kThreads) void permute_rank_kernel(
-    const int32_t* __restrict__ ids, int64_t R, int E, int k, int nbits, int64_t Upad,
-    const int32_t* __restrict__ uc, const int32_t* __restrict__ counts,
-    int32_t* __restrict__ offsets, int32_t* __restrict__ dest, int32_t* __restrict__ sorted_tok) {
-  __shared__ int32_t s_off[kMaxExperts];
-  __shared__ int32_t run[kWavesPerBlock][kMaxExperts];
+// Block b (units 4b .. 4b + 3) writes its per-expert totals to bc[e][b].
+__global__ __launch_bounds__(kThreads) void permute_count_kernel(const int32_t* __restrict__ ids,
+                                                                int64_t R, int E, int nbits,
+                                                                int64_t Bpad,
+                                                                int32_t* __restrict__ bc) {
+  __shared__ int32_t cnt[kWavesPerBlock][kMaxExperts];
   const int tid = threadIdx.x;
-  const int32_t c = tid < E ? counts[tid] : 0;
-  int32_t total;
-  const int32_t ex = block_exclusive_scan256(c, &total);
-  if (tid < E) s_off[tid] = ex;
-  if (blockIdx.x == 0) {
-    if (tid < E) offsets[tid] = ex;
-    if (tid == 0) offsets[E] = total;
-  }
-  __syncthreads();
   const int lane = tid & (kWave - 1);
   const int w = tid / kWave;
   const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + w;
-  for (int e = lane; e < E; e += kWave) run[w][e] = s_off[e] + uc[int64_t(e) * Upad + unit];
+  int idv[kIters];
+  load_unit_ids(ids, unit * kUnit, R, lane, idv);
+  for (int e = lane; e < E; e += kWave) cnt[w][e] = 0;
   __syncthreads();
-  const int64_t base = unit * kUnit;
+  count_unit(idv, nbits, lane, cnt[w]);
+  __syncthreads();
+  if (tid < E) {
+    int32_t c = 0;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) c += cnt[i][tid];
+    bc[int64_t(tid) * Bpad + blockIdx.x] = c;
+  }
+}
+
+// Scan and rank in one pass.  Every block's per-expert total is already in bc
+// (the count kernel), so a block's exclusive prefix over the blocks before it
+// needs no waiting on other blocks: it sums its predecessors' totals itself (the
+// aggregates a decoupled look-back reads), and the sum over all blocks gives the
+// expert totals, hence the offsets.  The threads of one expert (256 / E' of them,
+// E' = E rounded up to a power of two) split its row of bc, 16-byte loads of four
+// blocks each, all issued before they are summed.  The block then counts its own
+// four units again (ids already in registers) for the prefix inside the block.
+constexpr int kRowLoads = 8;                       // 16-byte loads in flight per thread
+
+__global__ __launch_bounds__(kThreads) void permute_rank_kernel(
+    const int32_t* __restrict__ ids, int64_t R, int E, int k, int nbits, int64_t B, int64_t Bpad,
+    const int32_t* __restrict__ bc, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ dest, int32_t* __restrict__ sorted_tok) {
+  __shared__ int32_t s_pre[kThreads];
+  __shared__ int32_t s_tot[kThreads];
+  __shared__ int32_t run[kWavesPerBlock][kMaxExperts];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int w = tid / kWave;
+  const int64_t b0 = blockIdx.x;
+  const int64_t unit = b0 * kWavesPerBlock + w;
+  int idv[kIters];
+  load_unit_ids(ids, unit * kUnit, R, lane, idv);
+  for (int e = lane; e < E; e += kWave) run[w][e] = 0;
+
+  // ---- per expert: totals of the blocks before this one, and of all blocks
+  const int tpe = kThreads >> nbits;                 // threads per expert (nbits <= 8)
+  const int e = tid / tpe, part = tid % tpe;
+  int32_t pre = 0, tot = 0;
+  if (e < E) {
+    const u32x4* row = reinterpret_cast<const u32x4*>(bc + int64_t(e) * Bpad);
+    const int64_t nvec = Bpad / 4;
+    for (int64_t v0 = part; v0 < nvec; v0 += int64_t(kRowLoads) * tpe) {
+      u32x4 q[kRowLoads];
+#pragma unroll
+      for (int j = 0; j < kRowLoads; ++j) {
+        const int64_t v = v0 + int64_t(j) * tpe;
+        q[j] = v < nvec ? row[v] : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int j = 0; j < kRowLoads; ++j) {
+        const int64_t v = v0 + int64_t(j) * tpe;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t b = 4 * v + i;
+          const int32_t c = b < B ? int32_t(q[j][i]) : 0;
+          tot += c;
+          pre += b < b0 ? c : 0;
+        }
+      }
+    }
+  }
+  s_pre[tid] = pre;
+  s_tot[tid] = tot;
+  __syncthreads();
+  count_unit(idv, nbits, lane, run[w]);            // this wave's own unit
+  // thread e (< E) gathers its expert's partial sums; the offsets are the
+  // exclusive scan of the totals over the experts
+  int32_t total_e = 0, pre_e = 0;
+  if (tid < E) {
+    for (int i = 0; i < tpe; ++i) {
+      total_e += s_tot[tid * tpe + i];
+      pre_e += s_pre[tid * tpe + i];
+    }
+  }
+  int32_t all;
+  const int32_t off_e = block_exclusive_scan256(total_e, &all);   // synchronizes the block
+  if (blockIdx.x == 0) {
+    if (tid < E) {
+      counts[tid] = total_e;
+      offsets[tid] = off_e;
+    }
+    if (tid == 0) offsets[E] = all;
+  }
+  // running row of each of the block's units: offset + blocks before this one +
+  // the block's own earlier units
+  if (tid < E) {
+    int32_t r = off_e + pre_e;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+      const int32_t c = run[i][tid];
+      run[i][tid] = r;
+      r += c;
+    }
+  }
+  __syncthreads();
   const uint64_t below = (1ull << lane) - 1ull;
+  const int64_t base = unit * kUnit;
+#pragma unroll
   for (int it = 0; it < kIters; ++it) {
     const int64_t a = base + it * kWave + lane;
-    const bool valid = a < R;
-    const int id = valid ? ids[a] : 0;
+    const bool valid = idv[it] >= 0;
+    const int id = valid ? idv[it] : 0;
     const uint64_t match = wave_match(id, valid, nbits);
     if (valid) {
       const int32_t r0 = run[w][id];
@@ -245,12 +321,13 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
     MOE_LAUNCH("permute_small", permute_small_kernel, dim3(1), dim3(kSmallThreads), s, ids, R, E, k, nbits,
                counts, offsets, dest, sorted_tok);
   } else {
-    const unsigned unit_blocks = unsigned(Upad / kWavesPerBlock);
-    MOE_LAUNCH("permute_count", permute_count_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E,
-               nbits, Upad, uc);
-    MOE_LAUNCH("permute_scan", permute_scan_kernel, dim3(E), dim3(kThreads), s, uc, U, Upad, counts);
-    MOE_LAUNCH("permute_rank", permute_rank_kernel, dim3(unit_blocks), dim3(kThreads), s, ids, R, E, k,
-               nbits, Upad, uc, counts, offsets, dest, sorted_tok);
+    // per-block totals [E][Bpad] in the workspace (E * Bpad <= E * Upad ints)
+    const int64_t B = Upad / kWavesPerBlock;
+    const int64_t Bpad = (B + 3) / 4 * 4;
+    MOE_LAUNCH("permute_count", permute_count_kernel, dim3(unsigned(B)), dim3(kThreads), s, ids, R, E, nbits,
+               Bpad, uc);
+    MOE_LAUNCH("permute_rank", permute_rank_kernel, dim3(unsigned(B)), dim3(kThreads), s, ids, R, E, k, nbits,
+               B, Bpad, uc, counts, offsets, dest, sorted_tok);
   }
   if (x_perm == nullptr) return hipGetLastError();     // maps only: the grouped FFN gathers rows
   const int64_t row_bytes = int64_t(H) * elt;
