@@ -143,6 +143,27 @@ moe_status moe_permute(const int32_t* topk_ids, const void* x, int64_t T, int32_
                        void* ws, size_t ws_bytes, moe_stream stream);
 
 /*
+ * moe_permute_static - moe_permute for callers that cannot allocate: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * takes no workspace and allocates nothing: its scratch (per-expert counts of
+ * blocks of assignments) is a static device array of
+ * MOE_PERMUTE_STATIC_SCRATCH_BYTES that the library holds on every device it
+ * runs on until the process ends.  Arguments, outputs and results are those of
+ * moe_permute, bit for bit.
+ *
+ * Calls that overlap on one device (e.g. on two streams) share that array and
+ * race; serialize them.  Nothing in the array needs clearing between calls.
+ * Errors: as moe_permute, without WORKSPACE_TOO_SMALL; UNSUPPORTED when
+ * moe_permute_workspace_bytes(T, E, k) exceeds MOE_PERMUTE_STATIC_SCRATCH_BYTES
+ * (4 MiB: e.g. up to 2^24 assignments with 64 experts, 2^22 with 256); HIP when
+ * the array's device address cannot be obtained.
+ */
+#define MOE_PERMUTE_STATIC_SCRATCH_BYTES (4u << 20)
+moe_status moe_permute_static(const int32_t* topk_ids, const void* x, int64_t T, int32_t E, int32_t k,
+                              int32_t H, moe_dtype dt, int32_t* expert_counts, int32_t* expert_offsets,
+                              int32_t* sorted_token_ids, int32_t* dest_rows, void* x_perm, moe_stream stream);
+
+/*
  * moe_grouped_ffn - every expert's SwiGLU FFN on its own rows, as one grouped
  * GEMM pair (the expert computation of the MoE module in Algorithm 1).
  *

@@ -17,7 +17,7 @@ import torch
 
 __all__ = [
     "MoEError", "lib", "LIB_PATH", "HEADER_PATH", "abi_version", "exported_symbols",
-    "moe_route", "moe_router_topk", "moe_permute", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
+    "moe_route", "moe_router_topk", "moe_permute", "moe_permute_static", "moe_grouped_ffn", "moe_grouped_ffn_gather", "moe_combine",
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
     "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
     "moe_grouped_ffn_mxfp8", "moe_grouped_ffn_mxfp8_gather", "MXFP8", "quantize_weights_mxfp8",
@@ -57,6 +57,8 @@ _SIGNATURES = {
     "moe_permute_workspace_bytes": (_SZ, [_I64, _I32, _I32]),
     "moe_permute": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P,
                                    _P, _SZ, _P]),
+    "moe_permute_static": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P,
+                                          _P]),
     "moe_grouped_ffn_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I32, ctypes.c_int]),
     "moe_grouped_ffn": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, ctypes.c_int, _P,
                                        _P, _SZ, _P]),
@@ -193,6 +195,25 @@ def moe_permute(topk_ids, x, E, out=None, ws=None, stream=None, gather_rows=True
     _check(lib().moe_permute(_ptr(topk_ids), _ptr(x), T, E, k, H, _dt(x), _ptr(out["counts"]),
                              _ptr(out["offsets"]), _ptr(out["sorted_token_ids"]), _ptr(out["dest_rows"]),
                              _ptr(out["x_perm"]), _ptr(ws), ws.numel(), _stream(stream, dev)))
+    return out
+
+
+def moe_permute_static(topk_ids, x, E, out=None, stream=None, gather_rows=True):
+    """moe_permute with the library's static device scratch instead of a workspace
+    (the call allocates nothing on the device) -> the same dict as moe_permute."""
+    T, k = topk_ids.shape
+    H = x.shape[1]
+    dev = x.device
+    if out is None:
+        out = dict(counts=torch.empty(E, dtype=torch.int32, device=dev),
+                   offsets=torch.empty(E + 1, dtype=torch.int32, device=dev),
+                   sorted_token_ids=torch.empty(T * k, dtype=torch.int32, device=dev),
+                   dest_rows=torch.empty((T, k), dtype=torch.int32, device=dev),
+                   x_perm=torch.empty((T * k, H), dtype=x.dtype, device=dev) if gather_rows else None)
+    _dev(topk_ids, x, *out.values())
+    _check(lib().moe_permute_static(_ptr(topk_ids), _ptr(x), T, E, k, H, _dt(x), _ptr(out["counts"]),
+                                    _ptr(out["offsets"]), _ptr(out["sorted_token_ids"]), _ptr(out["dest_rows"]),
+                                    _ptr(out["x_perm"]), _stream(stream, dev)))
     return out
 
 

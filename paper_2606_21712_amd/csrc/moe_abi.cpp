@@ -131,6 +131,22 @@ moe_status moe_permute(const int32_t* topk_ids, const void* x, int64_t T, int32_
                                         x_perm, static_cast<int32_t*>(ws), upad, stream_of(stream)));
 }
 
+moe_status moe_permute_static(const int32_t* topk_ids, const void* x, int64_t T, int32_t E, int32_t k,
+                              int32_t H, moe_dtype dt, int32_t* expert_counts, int32_t* expert_offsets,
+                              int32_t* sorted_token_ids, int32_t* dest_rows, void* x_perm, moe_stream stream) {
+  moe::Check c = moe::validate_permute_static(topk_ids, x, T, E, k, H, dt, expert_counts, expert_offsets,
+                                              sorted_token_ids, dest_rows, x_perm);
+  if (!c.ok() || T == 0) return finish(c);
+  void* ws = nullptr;
+  const hipError_t err = moe::permute_static_scratch(&ws);
+  if (err != hipSuccess) return hip_status("moe_permute_static", err);
+  const int64_t upad = (moe::permute_units(T * k) + 3) / 4 * 4;
+  return hip_status("moe_permute_static",
+                    moe::launch_permute(topk_ids, x, T, E, k, H, dt == MOE_DTYPE_F32 ? 4 : 2, expert_counts,
+                                        expert_offsets, sorted_token_ids, dest_rows, x_perm,
+                                        static_cast<int32_t*>(ws), upad, stream_of(stream)));
+}
+
 size_t moe_grouped_ffn_workspace_bytes(int64_t R, int32_t E, int32_t H, int32_t F, moe_dtype dt) {
   return moe::ffn_workspace_bytes(R, E, H, F, dt);
 }

@@ -31,6 +31,9 @@ hipError_t launch_route(const float* logits, int64_t T, int E, int k, int renorm
 hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, int k, int H, int elt,
                           int32_t* counts, int32_t* offsets, int32_t* sorted_tok, int32_t* dest,
                           void* x_perm, int32_t* unit_counts, int64_t units_padded, hipStream_t s);
+// Device address of the static scratch array of moe_permute_static on the current
+// device (kPermuteStaticScratchBytes, tiling.h); looked up once per device.
+hipError_t permute_static_scratch(void** out);
 
 // Grouped SwiGLU FFN (bf16).  act is x_perm [R, H], or with gather != null the
 // token rows x [T, H] read through gather[r] (T * H * 2 < 2^31).  Device scratch:

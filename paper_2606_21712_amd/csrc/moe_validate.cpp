@@ -173,6 +173,31 @@ Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, 
   return Check{};
 }
 
+Check validate_permute_static(const int32_t* ids, const void* x, int64_t T, int32_t E, int32_t k, int32_t H,
+                              int dt, const int32_t* counts, const int32_t* offsets, const int32_t* sorted_tok,
+                              const int32_t* dest, const void* x_perm) {
+  const char* fn = "moe_permute_static";
+  MOE_TRY(experts_topk(fn, E, k));
+  MOE_TRY(tokens(fn, T, k));
+  MOE_TRY(dim64(fn, "H", H));
+  MOE_TRY(dtype(fn, dt));
+  if (T == 0) return Check{};
+  MOE_TRY(ptr(fn, "expert_counts", counts));
+  MOE_TRY(ptr(fn, "expert_offsets", offsets));
+  MOE_TRY(ptr(fn, "topk_ids", ids));
+  MOE_TRY(ptr(fn, "sorted_token_ids", sorted_tok));
+  MOE_TRY(ptr(fn, "dest_rows", dest));
+  if (x_perm != nullptr) {
+    MOE_TRY(ptr(fn, "x", x));
+    MOE_TRY(ptr(fn, "x_perm", x_perm));
+  }
+  const size_t need = permute_workspace_bytes(T, E, k);
+  if (need > kPermuteStaticScratchBytes)
+    return fail(MOE_ERR_UNSUPPORTED, fn, "needs %lld bytes of scratch, more than the static %lld",
+                (long long)need, (long long)kPermuteStaticScratchBytes);
+  return Check{};
+}
+
 namespace {
 
 // Checks shared by both grouped-FFN entry points; `act` is x_perm or x.

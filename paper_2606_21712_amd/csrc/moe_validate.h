@@ -39,6 +39,9 @@ Check validate_router_topk(const void* x, const void* w, int64_t T, int32_t E, i
 Check validate_permute(const int32_t* ids, const void* x, int64_t T, int32_t E, int32_t k, int32_t H,
                        int dt, const int32_t* counts, const int32_t* offsets, const int32_t* sorted_tok,
                        const int32_t* dest, const void* x_perm, const void* ws, size_t ws_bytes);
+Check validate_permute_static(const int32_t* ids, const void* x, int64_t T, int32_t E, int32_t k, int32_t H,
+                              int dt, const int32_t* counts, const int32_t* offsets, const int32_t* sorted_tok,
+                              const int32_t* dest, const void* x_perm);
 Check validate_ffn(const void* x_perm, const int32_t* offsets, int64_t R, int32_t E, int32_t H,
                    int32_t F, const void* wg, const void* wu, const void* wd, int dt,
                    const void* y_perm, const void* ws, size_t ws_bytes);

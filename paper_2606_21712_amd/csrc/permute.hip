@@ -16,6 +16,8 @@
 //                                                                   dest_rows, sorted_token_ids
 //   copy  : one wavefront per token reads x[t] once and writes its k rows.
 // Batches of at most 16 units run count and rank as one single-block kernel.
+#include <mutex>
+
 #include "common.h"
 #include "moe_internal.h"
 
@@ -335,6 +337,41 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
   MOE_LAUNCH("permute_copy", permute_copy_kernel<4>, dim3(copy_blocks), dim3(kThreads), s,
              static_cast<const uint8_t*>(x), T, k, row_bytes, dest, static_cast<uint8_t*>(x_perm));
   return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------- static scratch
+// moe_permute_static: the per-block counts live in this file-scope device array
+// instead of a caller workspace, so the call allocates nothing.  Every device the
+// library runs on holds its own copy for the life of the process.  In host code
+// the name `scratch` is only a stand-in for the symbol, not a device address: the
+// address comes from hipGetSymbolAddress, taken once per device (with that device
+// current) and cached.  Nothing in it has to start at zero (the count kernel
+// writes every count the rank kernel reads); calls that overlap on one device
+// share the array and race.
+static __device__ __align__(256) uint8_t scratch[kPermuteStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t permute_static_scratch(void** out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return err;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace moe

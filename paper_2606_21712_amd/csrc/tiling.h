@@ -24,4 +24,9 @@ constexpr int kMaxTailPieces = 256;
 constexpr int kMaxTailSplit = 8;
 constexpr int kMinPieceSteps = 8;
 
+// moe_permute_static keeps its per-expert counts of blocks of assignments (the
+// moe_permute workspace) in a static device array of this size instead of a
+// caller workspace: calls whose moe_permute_workspace_bytes() exceeds it are refused.
+constexpr unsigned long kPermuteStaticScratchBytes = 4ul << 20;
+
 }  // namespace moe

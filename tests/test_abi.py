@@ -250,3 +250,17 @@ def test_binding_rejects_cpu_tensors():
     import torch
     with pytest.raises(ValueError):
         moe.moe_route(torch.zeros(4, 8), 2)
+
+
+def test_permute_static_validation(L):
+    def call(T=16, E=8, k=2, H=64, ids=P, xp=P, ws_ok=True):
+        return L.moe_permute_static(ids, P, T, E, k, H, 1, P, P, P, P, xp, S)
+    assert call(H=96) == INVALID
+    assert call(k=3, E=2) == INVALID
+    assert call(ids=None) == INVALID
+    # the static array holds 4 MiB of per-unit counts: 2^22 assignments over 256 experts fit,
+    # 1024 more do not
+    assert L.moe_permute_workspace_bytes((1 << 22) // 8, 256, 8) == 4 << 20
+    assert call(T=(1 << 22) // 8 + 128, E=256, k=8) == UNSUPPORTED
+    assert b"static" in L.moe_last_error()
+    assert call(T=0, ids=None, xp=None) == 0
