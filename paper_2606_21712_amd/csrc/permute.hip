@@ -301,10 +301,11 @@ __global__ __launch_bounds__(kThreads) void permute_copy_kernel(const uint8_t* _
 #pragma unroll
     for (int j = 0; j < kMaxTopK; ++j) {
       if (j < k) {
+        // x_perm is not read again here: nontemporal stores
         u32x4* dst = reinterpret_cast<u32x4*>(x_perm + int64_t(rows[j]) * row_bytes);
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
-          if (v + u * kWave < nvec) dst[v + u * kWave] = val[u];
+          if (v + u * kWave < nvec) __builtin_nontemporal_store(val[u], dst + v + u * kWave);
       }
     }
   }
@@ -334,7 +335,7 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
   if (x_perm == nullptr) return hipGetLastError();     // maps only: the grouped FFN gathers rows
   const int64_t row_bytes = int64_t(H) * elt;
   const unsigned copy_blocks = unsigned((T + kWavesPerBlock - 1) / kWavesPerBlock);
-  MOE_LAUNCH("permute_copy", permute_copy_kernel<4>, dim3(copy_blocks), dim3(kThreads), s,
+  MOE_LAUNCH("permute_copy", permute_copy_kernel<8>, dim3(copy_blocks), dim3(kThreads), s,
              static_cast<const uint8_t*>(x), T, k, row_bytes, dest, static_cast<uint8_t*>(x_perm));
   return hipGetLastError();
 }
