@@ -199,14 +199,14 @@ moe_status moe_grouped_ffn(const void* x_perm, const int32_t* expert_offsets, in
  * result as moe_permute's x_perm followed by moe_grouped_ffn, bit for bit, but
  * the grouped copy of the activations (T*k rows) is never written or read.
  *
- *   x                 dt  [T, H]   token rows (T * H * element size < 2^31)
+ *   x                 dt  [T, H]   token rows (any size)
  *   sorted_token_ids  i32 [R]      from moe_permute (R = T*k)
  *   other arguments as moe_grouped_ffn; the workspace size is
  *   moe_grouped_ffn_workspace_bytes(R, E, H, F, dt)
  *
  * Errors: as moe_grouped_ffn, plus INVALID_ARGUMENT for T < 0, R > 0 with
- * T = 0, a NULL or misaligned x or sorted_token_ids; UNSUPPORTED when x is
- * 2 GiB or larger.  Token ids are not checked (precondition: 0 <= id < T).
+ * T = 0, a NULL or misaligned x or sorted_token_ids.  Token ids are not checked
+ * (precondition: 0 <= id < T).
  */
 moe_status moe_grouped_ffn_gather(const void* x, const int32_t* sorted_token_ids,
                                   const int32_t* expert_offsets, int64_t T, int64_t R, int32_t E,

@@ -91,7 +91,7 @@ struct GemmArgs {
   const int32_t* offsets;         // [E + 1]
   const int32_t* mtile_prefix;    // [E + 1]
   int E, K, N, ntiles, R;
-  int act_bytes;                  // bytes of act (gather only; < 2^31)
+  int act_bytes;                  // bytes of act (kTokens gather only; < 2^31)
 };
 
 // First tile row of a wavefront's n-subtile ni (0..1).  GEMM-1: ni = 0 is 32
@@ -113,9 +113,17 @@ constexpr int kWaitVm0 = 0x0F70;
 // Buffer resource word 3 for raw (unformatted, stride 0) buffer loads on gfx9.
 constexpr int kBufFlags = 0x00020000;
 
-// GATHER: activation row r of the tile list is row gather[r] of act (the token
-// rows themselves), so the grouped copy of the activations is never written.
-template <bool SWIGLU, bool GATHER>
+// Where the activation rows come from.
+enum Gather : int {
+  kRows = 0,       // act is the grouped rows [R, K]
+  kTokens = 1,     // row r is token row gather[r] of act [T, K], act < 2 GiB: one buffer
+                   // resource over all of act, 32-bit row offsets
+  kTokensWide = 2  // the same for act of any size: 64-bit per-lane row addresses
+};
+
+// GATHER != kRows: activation row r of the tile list is row gather[r] of act (the
+// token rows themselves), so the grouped copy of the activations is never written.
+template <bool SWIGLU, int GATHER>
 __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(GemmArgs p) {
   // Two pipeline stages, each [weight tile | activation tile].  They are filled by
   // direct global->LDS loads; two distinct objects let the compiler tell them apart.
@@ -193,9 +201,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     const int wrows = SWIGLU ? min(128, N - n0) : min(256, N - n0);
     const int64_t rowb = int64_t(K) * 2;
     const __amdgpu_buffer_rsrc_t ra =
-        GATHER ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.act), 0, p.act_bytes, kBufFlags)
-               : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.act) + int64_t(row0) * K, 0,
-                                                   int(arows * rowb), kBufFlags);
+        GATHER == kTokens
+            ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.act), 0, p.act_bytes, kBufFlags)
+            : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.act) + int64_t(row0) * K, 0,
+                                                int(arows * rowb), kBufFlags);
     const int64_t wfirst = (int64_t(e) * N + n0) * K;
     const __amdgpu_buffer_rsrc_t rw0 = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
@@ -203,14 +212,22 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
         const_cast<uint16_t*>(SWIGLU ? p.w1 : p.w0) + wfirst, 0, int(wrows * rowb), kBufFlags);
     // Per-lane byte offsets of the DMA passes (constant over the k loop).
     uint32_t aoff[5], woff[4];
+    const uint8_t* aptr[5];                 // kTokensWide: the lane's row address
 #pragma unroll
     for (int i = 0; i < 5; ++i) {
       const int r = (8 * i + wave) * 8 + qrow;                  // activation row this lane fills
       const uint32_t cb = uint32_t(swz(r, qpos) * 16);          // its logical chunk, in bytes
-      if (GATHER) {
+      const int grow = row0 + r;
+      if (GATHER == kTokens) {
         // The token's row; rows past the tile get an offset beyond num_records.
-        const int grow = row0 + r;
         aoff[i] = grow < row_stop ? uint32_t(p.gather[grow]) * uint32_t(rowb) + cb : 0x80000000u;
+      } else if (GATHER == kTokensWide) {
+        // No bounds check on these loads: a row past the tile reads the tile's first
+        // token row instead, whose products land only in output rows that are
+        // never stored.
+        const int64_t tok = p.gather[grow < row_stop ? grow : row0];
+        aptr[i] = reinterpret_cast<const uint8_t*>(p.act) + tok * rowb + cb;
+        aoff[i] = 0;
       } else {
         aoff[i] = uint32_t(r) * uint32_t(rowb) + cb;
       }
@@ -238,8 +255,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
 #pragma unroll
       for (int i = 0; i < 5; ++i) {
         const int blk = 8 * i + wave;
-        if (blk * 8 < arows)
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kWOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
+        if (blk * 8 < arows) {
+          if (GATHER == kTokensWide)
+            __builtin_amdgcn_global_load_lds(aptr[i] + kb, stage + kWOpBytes + blk * 1024, 16, 0, 0);
+          else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, stage + kWOpBytes + blk * 1024, 16, aoff[i], kb, 0, 0);
+        }
       }
     };
 
@@ -593,17 +614,22 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
              mtile_prefix, queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
+  const int64_t act_bytes = T * H * 2;
+  const bool wide = act_bytes >= (int64_t(1) << 31);
   GemmArgs a1{queues, act, gather, wg, wu, h, nullptr, offsets, mtile_prefix, E, H, F, (F + 127) / 128,
-              int(R), int(T * H * 2)};
+              int(R), wide ? 0 : int(act_bytes)};
   const dim3 grid1(grid_for(mtiles_upper * a1.ntiles, num_cu));
-  if (gather != nullptr)
-    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, true>), grid1, dim3(kGemmThreads), s, a1);
+  if (gather != nullptr && wide)
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, kTokensWide>), grid1, dim3(kGemmThreads), s,
+               a1);
+  else if (gather != nullptr)
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, kTokens>), grid1, dim3(kGemmThreads), s, a1);
   else
-    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, false>), grid1, dim3(kGemmThreads), s, a1);
+    MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_bf16_kernel<true, kRows>), grid1, dim3(kGemmThreads), s, a1);
   GemmArgs a2{queues + 1, h, nullptr, wd, nullptr, y_perm, partial, offsets, mtile_prefix, E, F, H,
               (H + 255) / 256, int(R), 0};
   const int grid2 = grid_for(mtiles_upper * a2.ntiles, num_cu);
-  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_bf16_kernel<false, false>), dim3(grid2), dim3(kGemmThreads), s,
+  MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_bf16_kernel<false, kRows>), dim3(grid2), dim3(kGemmThreads), s,
              a2);
   const hipError_t err = launch_tail_reduce(partial, mtile_prefix, offsets, E, a2.ntiles, grid2, F / kBK, H,
                                             y_perm, s);

@@ -36,7 +36,8 @@ hipError_t launch_permute(const int32_t* ids, const void* x, int64_t T, int E, i
 hipError_t permute_static_scratch(void** out);
 
 // Grouped SwiGLU FFN (bf16).  act is x_perm [R, H], or with gather != null the
-// token rows x [T, H] read through gather[r] (T * H * 2 < 2^31).  Device scratch:
+// token rows x [T, H] read through gather[r] (any size: x of 2 GiB or more is
+// read with 64-bit per-lane row addresses instead of one buffer resource).  Device scratch:
 // mtile_prefix (E + 1 ints), queues (2 ints), h [R, F], and the down
 // projection's tail-split partial slots (ffn_tail_partial_bytes); all are
 // rewritten by the call before use.

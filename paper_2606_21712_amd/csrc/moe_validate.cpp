@@ -246,9 +246,6 @@ Check validate_ffn_gather(const void* x, const int32_t* sorted_tok, int64_t T, c
   if (R > 0 && T == 0) return fail(MOE_ERR_INVALID_ARGUMENT, fn, "R=%lld rows but T=0 tokens", R);
   MOE_TRY(ffn_common(fn, "x", x, offsets, R, E, H, F, wg, wu, wd, dt, y_perm, ws, ws_bytes));
   if (R == 0) return Check{};
-  // The gathered rows are addressed with 32-bit byte offsets into x.
-  if (T * int64_t(H) * int64_t(elt(dt)) >= (int64_t(1) << 31))
-    return fail(MOE_ERR_UNSUPPORTED, fn, "x of T=%lld rows exceeds 2 GiB for the gather", T);
   MOE_TRY(ptr(fn, "sorted_token_ids", sorted_tok));
   return Check{};
 }
