@@ -339,15 +339,46 @@ SWEEP_SHAPES = {
     "mixtral": ("mixtral4k", 65536),
     "deepseek": ("deepseek", 32768),
     "memconstrained": ("memconstrained", 131072),
+    "memconstrained_lognormal": ("memconstrained", 131072),
 }
+
+
+def fit_ffn_model(rows, weight_bytes: float):
+    """Fit t_ffn(T) = t0 + max(weight_bytes / BW, flops(T) / P) to the measured
+    grouped-FFN times (least squares on the relative residuals): a fixed cost, the
+    expert weights streamed once at bandwidth BW, and the flops at rate P, the
+    larger of the two bounding each batch (the roofline of one grouped FFN).
+    Returns the parameters, the batch where the two bounds meet and each size's
+    residual."""
+    from scipy.optimize import least_squares
+    t = np.array([r["ffn_ms"] * 1e-3 for r in rows])
+    fl = np.array([r["flops"] for r in rows])
+
+    def model(q):
+        t0, bw, pf = np.exp(q)
+        return t0 + np.maximum(weight_bytes / bw, fl / pf)
+
+    q0 = np.log([1e-5, 5e12, 1.2e15])
+    res = least_squares(lambda q: model(q) / t - 1.0, q0)
+    t0, bw, pf = np.exp(res.x)
+    pred = model(res.x)
+    ridge_flops = weight_bytes / bw * pf
+    return dict(t0_us=round(t0 * 1e6, 2), weight_GBps=round(bw / 1e9, 1), tflops=round(pf / 1e12, 1),
+                ridge_flops=ridge_flops,
+                residual_pct=[round(100 * (p / m - 1.0), 2) for p, m in zip(pred, t)],
+                max_abs_residual_pct=round(100 * float(np.max(np.abs(pred / t - 1.0))), 2))
 
 
 def expert_batch_sweep(shape: str, steps: int, warmup: int):
     """Module-level roofline of the MoE layer: time one layer over expert batches of
-    T = 256 .. T_max tokens (the leading T tokens of one seeded batch, so every
-    smaller batch is a prefix of the larger ones) and report tokens/s and grouped
-    FFN TFLOP/s per size.  The saturation batch is the smallest T whose FFN
-    throughput reaches 90% of the largest measured."""
+    T = 256 .. T_max tokens and report tokens/s and grouped-FFN TFLOP/s per size,
+    then fit the grouped FFN's runtime model (fit_ffn_model).  Router-logit shapes
+    use the leading T tokens of one seeded batch (every smaller batch is a prefix of
+    the larger ones).  memconstrained_lognormal keeps the workload's own routing at
+    every T: exact per-expert counts from the same 64 lognormal(0, 1) draws, scaled
+    to T * k assignments, the three smallest experts pinned to 1, 17 and 31 rows.
+    The saturation batch is the smallest T whose FFN throughput reaches 90% of the
+    largest measured."""
     import torch
 
     import moegen
@@ -355,18 +386,31 @@ def expert_batch_sweep(shape: str, steps: int, warmup: int):
 
     name, tmax = SWEEP_SHAPES[shape]
     base = moegen.CONFIGS[name]
-    cfg = base.scaled(T=tmax, routing="router") if base.routing != "router" else base.scaled(T=tmax)
+    lognormal = shape == "memconstrained_lognormal"
+    cfg = base.scaled(T=tmax) if lognormal or base.routing == "router" else base.scaled(T=tmax, routing="router")
     log(f"sweep {shape}: generating T={cfg.T} H={cfg.H} E={cfg.E} k={cfg.k} F={cfg.F} Fs={cfg.Fs}")
     I = moegen.make_inputs(cfg)
-    x, logits = to_dev(I.x, torch), to_dev(I.logits, torch)
+    x = to_dev(I.x, torch)
+    logits_all = to_dev(I.logits, torch)
     wg, wu, wd = to_dev(I.w_gate, torch), to_dev(I.w_up, torch), to_dev(I.w_down, torch)
     shared = (to_dev(I.ws_gate, torch), to_dev(I.ws_up, torch), to_dev(I.ws_down, torch)) if cfg.Fs \
         else (None, None, None)
+    w_r = moegen.router_matrix(cfg) if lognormal else None
     rows = []
     T = 256
     while T <= tmax:
-        layer = moe.MoELayer(T, cfg.H, cfg.E, cfg.k, cfg.F, cfg.Fs)
-        xs, ls = x[:T].contiguous(), logits[:T].contiguous()
+        layer = moe.MoELayer(T, cfg.H, cfg.E, cfg.k, cfg.F, cfg.Fs, gather=True)
+        xs = x[:T].contiguous()
+        if lognormal:
+            # the workload's routing recipe at this T (generator only: counts, sets, margin logits)
+            rng = np.random.default_rng(np.random.SeedSequence([cfg.seed, T]))
+            target = moegen.lognormal_counts(rng, cfg.E, T * cfg.k, cfg.lognormal_sigma, cfg.pinned_small)
+            chosen, _ = moegen.exact_count_assignment(target, T, cfg.k, rng)
+            ls = to_dev(moegen.margin_logits(I.x[:T], w_r, chosen, cfg.margin), torch)
+            counts = np.sort(np.bincount(chosen.ravel(), minlength=cfg.E))
+        else:
+            ls = logits_all[:T].contiguous()
+            counts = None
 
         def step():
             layer.run(xs, ls, wg, wu, wd, *shared, renormalize=cfg.renormalize)
@@ -391,16 +435,26 @@ def expert_batch_sweep(shape: str, steps: int, warmup: int):
         flops = 6.0 * cfg.H * cfg.F * T * cfg.k + 6.0 * cfg.H * cfg.Fs * T
         row = {"tokens": T, "ms_per_layer": round(ms, 4), "tokens_per_s": round(T / ms * 1e3, 1),
                "ffn_ms": round(ffn_ms, 4), "ffn_tflops": round(flops / ffn_ms / 1e9, 1),
-               "tokens_per_expert": T * cfg.k / cfg.E}
+               "tokens_per_expert": T * cfg.k / cfg.E, "flops": flops}
+        if counts is not None:
+            row["smallest_groups"] = counts[:3].tolist()
+            row["largest_group"] = int(counts[-1])
         rows.append(row)
         print(json.dumps({"sweep": shape, **row}), flush=True)
         del layer
         T *= 2
     peak = max(r["ffn_tflops"] for r in rows)
     sat = next(r["tokens"] for r in rows if r["ffn_tflops"] >= 0.9 * peak)
+    weight_bytes = 3.0 * cfg.E * cfg.H * cfg.F * 2 + 3.0 * cfg.H * cfg.Fs * 2
+    fit = fit_ffn_model(rows, weight_bytes)
+    ridge_T = fit.pop("ridge_flops") / (6.0 * cfg.H * (cfg.F * cfg.k + cfg.Fs))
     print(json.dumps({"sweep": shape, "summary": True, "peak_ffn_tflops": peak,
                       "saturation_tokens_90pct": sat,
-                      "saturation_tokens_per_expert": sat * cfg.k / cfg.E}), flush=True)
+                      "saturation_tokens_per_expert": sat * cfg.k / cfg.E,
+                      "model": "t_ffn(T) = t0 + max(weight_bytes / BW, flops(T) / P)",
+                      "weight_bytes": weight_bytes, **fit,
+                      "ridge_tokens": round(ridge_T, 1),
+                      "ridge_tokens_per_expert": round(ridge_T * cfg.k / cfg.E, 1)}), flush=True)
 
 
 # --------------------------------------------------------------------------- algorithmic work per kernel
@@ -659,6 +713,47 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
     print("\n".join(lines))
 
 
+def summarize_probe(root):
+    """Counters per kernel instantiation (full template name) from the --pmc passes
+    under root, for the stand-alone probes (--route-probe): duration, VALU
+    instructions and the share of the SIMDs' issue cycles they fill (a wave64 VALU
+    instruction holds its SIMD 4 cycles), wave-cycles spent waiting, bytes."""
+    import glob
+    import re
+    per = {}
+    for path in sorted(glob.glob(os.path.join(root, "*", "*counter_collection.csv"))):
+        if os.path.basename(os.path.dirname(path)).startswith("copy_"):
+            continue
+        by_disp = {}
+        for r in _read_csv(path):
+            d = by_disp.setdefault(int(r["Dispatch_Id"]), dict(name=r["Kernel_Name"], counters={}))
+            d["counters"][r["Counter_Name"]] = float(r["Counter_Value"])
+            d["us"] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        for d in by_disp.values():
+            m = re.search(r"(\w+_kernel<[^()]*>)", d["name"])
+            if not m or not m.group(1).startswith(("route_kernel", "router_")):
+                continue
+            slot = per.setdefault(m.group(1), {})
+            for k, v in d["counters"].items():
+                slot.setdefault(k, []).append(v)
+            slot.setdefault("us", []).append(d["us"])
+    lines = ["| kernel | dispatches | us (pmc run) | VALU instr | VALU issue share % | wave-cycles waiting % | "
+             "FETCH_SIZE KiB | WRITE_SIZE KiB |", "|---|---|---|---|---|---|---|---|"]
+    for name, sl in per.items():
+        m = {k: float(np.median(v)) for k, v in sl.items()}
+        cyc = m.get("GRBM_GUI_ACTIVE", 0) / NUM_XCD
+        valu = m.get("SQ_INSTS_VALU")
+        share = 100 * valu * 4 / (cyc * NUM_SIMD) if valu and cyc else None
+        wait = 100 * m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"] if m.get("SQ_WAVE_CYCLES") and "SQ_WAIT_ANY" in m \
+            else None
+
+        def f(v, fmt):
+            return "-" if v is None else format(v, fmt)
+        lines.append(f"| `{name}` | {len(sl['us'])} | {m['us']:.1f} | {f(valu, '.3g')} | {f(share, '.1f')} | "
+                     f"{f(wait, '.1f')} | {f(m.get('FETCH_SIZE'), '.0f')} | {f(m.get('WRITE_SIZE'), '.0f')} |")
+    print("\n".join(lines))
+
+
 def main():
     import moegen
 
@@ -677,9 +772,11 @@ def main():
     ap.add_argument("--summarize", metavar="DIR", default=None,
                     help="print markdown tables from the rocprofv3 output under DIR (kernel traces and "
                          "counter passes of --profile-run / default runs of --config)")
+    ap.add_argument("--probe", action="store_true",
+                    help="with --summarize: counters per kernel instantiation of a --route-probe run")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
-    ap.add_argument("--sweep", choices=["mixtral", "deepseek", "memconstrained"], default=None,
+    ap.add_argument("--sweep", choices=sorted(SWEEP_SHAPES), default=None,
                     help="expert-batch sweep of one layer shape: one JSON line per batch size")
     ap.add_argument("--mxfp8", action="store_true",
                     help="time the layer with MXFP8 expert GEMMs on --config (a separate JSON line)")
@@ -688,6 +785,8 @@ def main():
     ap.add_argument("--route-probe", action="store_true",
                     help="only time moe_route at 2^20 tokens (bandwidth probe), cold and warm")
     args = ap.parse_args()
+    if args.summarize and args.probe:
+        return summarize_probe(args.summarize)
     if args.summarize:
         return summarize(args.summarize, moegen.CONFIGS[args.config], args.warmup, args.steps,
                          gather=not args.no_gather)

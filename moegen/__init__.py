@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "MoEConfig", "CONFIGS", "Inputs", "make_inputs", "round_bf16", "as_f64",
-    "zipf_counts", "lognormal_counts", "exact_count_assignment",
+    "zipf_counts", "lognormal_counts", "exact_count_assignment", "router_matrix", "margin_logits",
 ]
 
 _CHUNK = 1 << 22          # elements per independently seeded chunk
@@ -229,6 +229,21 @@ def _router_logits(x: np.ndarray, w_r: np.ndarray, bias: np.ndarray | None) -> n
             acc += bias[lo:hi]
         out[lo:hi] = acc.astype(np.float32)
     return out
+
+
+def router_matrix(cfg: MoEConfig) -> np.ndarray:
+    """The router matrix W_r [H, E] fp32 of the workload's seed (the same draw as
+    make_inputs)."""
+    s_r = np.random.SeedSequence(cfg.seed).spawn(9)[1]
+    return _normal(s_r, (cfg.H, cfg.E), cfg.router_std, "f32")
+
+
+def margin_logits(x: np.ndarray, w_r: np.ndarray, chosen: np.ndarray, margin: float) -> np.ndarray:
+    """fp32(x . W_r + margin on each token's chosen experts): logits whose top-k is
+    exactly the chosen set when the margin exceeds the spread of x . W_r."""
+    mark = np.zeros((x.shape[0], w_r.shape[1]), dtype=np.float64)
+    np.put_along_axis(mark, np.asarray(chosen, dtype=np.int64), margin, axis=1)
+    return _router_logits(x, w_r, mark)
 
 
 def make_inputs(cfg: MoEConfig | str, seed: int | None = None, with_weights: bool = True) -> Inputs:
