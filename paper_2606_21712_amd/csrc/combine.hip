@@ -1,8 +1,9 @@
 // moe_combine: y[t] = sum_j w[t,j] * y_perm[dest_rows[t,j]] (+ y_shared[t]) on gfx950.
 //
-// Gather form: one wavefront per token walks the hidden dimension in 16-byte
-// vectors (8 bf16 or 4 fp32 per lane), loads the token's k expert rows, sums
-// them in fp32 in slot order, adds the shared-expert row last and rounds once.
+// Gather form: one wavefront per token (or per part of a token's row, for large
+// batches) walks the hidden dimension in 16-byte vectors (8 bf16 or 4 fp32 per
+// lane), loads the token's k expert rows, sums them in fp32 in slot order, adds
+// the shared-expert row last and rounds once.
 // For k = 1, 2, 4, 8 the loads of all k rows are in flight together, up to 32
 // sixteen-byte loads per lane; y is stored with nontemporal stores.
 // Every output element is written by exactly one lane, so there are no atomics
@@ -60,13 +61,15 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __rest
                                                           const int32_t* __restrict__ dest,
                                                           const float* __restrict__ w,
                                                           const uint8_t* __restrict__ y_shared,
-                                                          int64_t T, int k, int64_t row_bytes,
+                                                          int64_t T, int k, int64_t row_bytes, int splits,
                                                           uint8_t* __restrict__ y) {
   using V = Vec<BF16>;
   constexpr int KM = KT > 0 ? KT : kMaxTopK;
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int64_t t = int64_t(blockIdx.x) * kWavesPerBlock + wv;
+  const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
+  const int64_t t = gw / splits;
+  const int part = int(gw % splits);
   if (t >= T) return;
   if (KT > 0) k = KT;
   int32_t rows[KM];
@@ -76,8 +79,10 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __rest
     rows[j] = j < k ? dest[t * k + j] : 0;
     wt[j] = j < k ? w[t * k + j] : 0.f;
   }
-  const int nvec = int(row_bytes / 16);
-  for (int v0 = lane; v0 < nvec; v0 += kWave * UNROLL) {
+  const int nall = int(row_bytes / 16);
+  const int vlo = part * nall / splits;
+  const int nvec = (part + 1) * nall / splits;
+  for (int v0 = vlo + lane; v0 < nvec; v0 += kWave * UNROLL) {
     float acc[UNROLL][V::N];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
@@ -147,28 +152,28 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint8_t* __rest
 
 template <bool BF16>
 void launch_combine_t(const uint8_t* yp, const int32_t* dest, const float* w, const uint8_t* ys, int64_t T,
-                      int k, int64_t row_bytes, uint8_t* yo, unsigned blocks, hipStream_t s) {
+                      int k, int64_t row_bytes, int splits, uint8_t* yo, unsigned blocks, hipStream_t s) {
   // 32 (k = 1, 2: 8 or 16) sixteen-byte loads in flight per lane: k rows x UNROLL vectors.
   switch (k) {
     case 1:
       MOE_LAUNCH("combine", (combine_kernel<BF16, 1, 8>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
-                 k, row_bytes, yo);
+                 k, row_bytes, splits, yo);
       break;
     case 2:
       MOE_LAUNCH("combine", (combine_kernel<BF16, 2, 8>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
-                 k, row_bytes, yo);
+                 k, row_bytes, splits, yo);
       break;
     case 4:
       MOE_LAUNCH("combine", (combine_kernel<BF16, 4, 8>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
-                 k, row_bytes, yo);
+                 k, row_bytes, splits, yo);
       break;
     case 8:
       MOE_LAUNCH("combine", (combine_kernel<BF16, 8, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
-                 k, row_bytes, yo);
+                 k, row_bytes, splits, yo);
       break;
     default:
       MOE_LAUNCH("combine", (combine_kernel<BF16, 0, 2>), dim3(blocks), dim3(kThreads), s, yp, dest, w, ys, T,
-                 k, row_bytes, yo);
+                 k, row_bytes, splits, yo);
   }
 }
 
@@ -177,14 +182,25 @@ void launch_combine_t(const uint8_t* yp, const int32_t* dest, const float* w, co
 hipError_t launch_combine(const void* y_perm, const int32_t* dest, const float* w, const void* y_shared,
                           int64_t T, int k, int H, bool bf16, void* y, hipStream_t s) {
   const int64_t row_bytes = int64_t(H) * (bf16 ? 2 : 4);
-  const unsigned blocks = unsigned((T + kWavesPerBlock - 1) / kWavesPerBlock);
+  const int nvec = int(row_bytes / 16);
+  // Column split: a token's row is cut into `splits` parts, one wavefront each, so
+  // that large batches run enough wavefronts with a few vectors per lane each
+  // (measured cold, % of 8 TB/s: memory-constrained 71 -> 76 with 2 parts,
+  // Mixtral-shaped 32K tokens 75 -> 77 with 4, DeepSeek-shaped 65 -> 70 with 8);
+  // small batches (fewer than 8192 tokens) keep whole rows.
+  int splits = 1;
+  if (T >= 8192)
+    while (splits < 8 && nvec / (2 * splits) >= kWave && T * splits < (int64_t(1) << 30) &&
+           (nvec / splits > 4 * kWave || T * splits < 131072))
+      splits *= 2;
+  const unsigned blocks = unsigned((T * splits + kWavesPerBlock - 1) / kWavesPerBlock);
   auto yp = static_cast<const uint8_t*>(y_perm);
   auto ys = static_cast<const uint8_t*>(y_shared);
   auto yo = static_cast<uint8_t*>(y);
   if (bf16)
-    launch_combine_t<true>(yp, dest, w, ys, T, k, row_bytes, yo, blocks, s);
+    launch_combine_t<true>(yp, dest, w, ys, T, k, row_bytes, splits, yo, blocks, s);
   else
-    launch_combine_t<false>(yp, dest, w, ys, T, k, row_bytes, yo, blocks, s);
+    launch_combine_t<false>(yp, dest, w, ys, T, k, row_bytes, splits, yo, blocks, s);
   return hipGetLastError();
 }
 

@@ -290,11 +290,16 @@ def test_combine_direct():
     rng = np.random.default_rng(7)
     # k = 1, 2, 4, 8 take the kernels with every row's loads in flight, other k the
     # generic one; H = 4160 needs two passes of the widest unroll, with a ragged tail.
+    # Batches of 8192 tokens and more cut each row into parts of one wavefront each:
+    # 4 parts of 112 vectors (H = 3584, a ragged pass per lane), 8 parts (H = 8192),
+    # 4 parts in fp32 (H = 1024).
     for (T, k, H, shared, bf16) in [(999, 4, 192, True, True), (64, 16, 64, False, True),
                                     (1, 1, 128, True, True), (77, 8, 576, True, True),
                                     (50, 2, 4160, False, True), (33, 1, 1024, True, True),
                                     (41, 3, 320, True, True), (90, 8, 704, True, False),
-                                    (37, 2, 4160, True, False), (20, 5, 64, False, False)]:
+                                    (37, 2, 4160, True, False), (20, 5, 64, False, False),
+                                    (8192, 4, 3584, True, True), (8192, 2, 8192, False, True),
+                                    (9000, 1, 1024, True, False)]:
         R = T * k
         cast = moegen.round_bf16 if bf16 else (lambda a: a)
         yp = cast(rng.standard_normal((R, H)).astype(np.float32))
