@@ -71,12 +71,26 @@ __global__ __launch_bounds__(64) void router_kernel(const uint16_t* __restrict__
     wv[nb] = nb * 16 + r16 < E;
     wr[nb] = reinterpret_cast<const bf16x8*>(w + int64_t(wv[nb] ? nb * 16 + r16 : 0) * H + kq * 8);
   }
-  f32x4 acc[MB][NB];
+  f32x4 acc[MB][NB], tot[MB][NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bf16x8 zero = {};
+  // k order of the sum (the same in every router kernel, so a token's logits do not
+  // depend on the batch it arrives in): with H % 128 = 0, four quarter sums over
+  // consecutive 32-k chunks, added as ((q0 + q1) + q2) + q3; otherwise one chain.
+  const int qc = (H % 128 == 0) ? H / 128 : 0;         // 32-k chunks per quarter
+  auto fold = [&](int c) {                              // before chunk c
+    if (qc == 0 || c == 0 || c % qc != 0) return;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        tot[mb][nb] = c == qc ? acc[mb][nb] : tot[mb][nb] + acc[mb][nb];
+        acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+  };
 
   // k-steps of 32: operand vector index k0 / 8 (each bf16x8 covers 8 of k)
   constexpr int U = MB * NB > 8 ? 2 : kUnroll;        // keep the operands in flight in registers
@@ -92,14 +106,17 @@ __global__ __launch_bounds__(64) void router_kernel(const uint16_t* __restrict__
       for (int nb = 0; nb < NB; ++nb) b[u][nb] = wv[nb] ? wr[nb][(k0 + 32 * u) / 8] : zero;
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      fold((k0 + 32 * u) / 32);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
           acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][mb], b[u][nb], acc[mb][nb], 0, 0, 0);
+    }
   }
   for (; k0 < H; k0 += 32) {
+    fold(k0 / 32);
     bf16x8 b[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) b[nb] = wv[nb] ? wr[nb][k0 / 8] : zero;
@@ -112,6 +129,12 @@ __global__ __launch_bounds__(64) void router_kernel(const uint16_t* __restrict__
     }
   }
 
+  if (qc != 0) {                                        // the last quarter
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = tot[mb][nb] + acc[mb][nb];
+  }
   // 16 x 16 output: lane holds tokens 4 (lane / 16) + q of expert block column lane % 16
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -266,12 +289,22 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
       a[u] = xv ? __builtin_nontemporal_load(xr + (s * kSliceK + 32 * u) / 8) : zero;
   };
 
-  f32x4 acc[NB];
+  f32x4 acc[NB], tot[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](const uint8_t* slice, const bf16x8* a) {
+  // k order as router_kernel: four quarter sums, added ((q0 + q1) + q2) + q3
+  const int qc = H / 128;                             // 32-k chunks per quarter
+  auto compute = [&](const uint8_t* slice, const bf16x8* a, int s) {
 #pragma unroll
     for (int u = 0; u < kSliceSteps; ++u) {
+      const int c = s * kSliceSteps + u;
+      if (c != 0 && c % qc == 0) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          tot[nb] = c == qc ? acc[nb] : tot[nb] + acc[nb];
+          acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         const int row = nb * 16 + r16;
@@ -293,7 +326,7 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
       issue_w(nxt, s + 1);
       load_x(a_nxt, s + 1);
     }
-    compute(cur, a_cur);
+    compute(cur, a_cur, s);
   };
   int s = 0;
   for (; s + 2 <= S; s += 2) {
@@ -301,6 +334,8 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
     step(ws1, ws0, xa[1], xa[0], s + 1);
   }
   if (s < S) step(ws0, ws1, xa[0], xa[1], s);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = tot[nb] + acc[nb];   // the last quarter
 
   // 16 x 16 outputs: lane holds tokens 4 (lane / 16) + q of expert column lane % 16
 #pragma unroll

@@ -93,3 +93,34 @@ def test_router_workload(name):
     frac = check(I.x, I.extra["w_router"], c.k)
     log(f"[gpu]   {frac:.4f} of the tokens checked against the exact logits' routing")
     assert frac > 0.95          # 64 experts, top-8: ~97% of tokens clear twice the bound
+
+
+@pytest.mark.parametrize("H,sizes", [(640, (100, 600, 1100, 2100)), (1024, (100, 300)), (192, (100, 600, 1100, 2100))])
+def test_router_batch_size_invariant(H, sizes):
+    """The same tokens routed in batches of different sizes get bitwise-identical
+    logits, ids and weights: every kernel variant (k split four ways for small
+    batches, LDS-staged router matrix, 16 / 32 / 64 tokens per wavefront) adds the
+    products in the same k order.  A budget of 4 compute units puts the variants'
+    switch points at small T: with H = 640 the sizes run split-k, then 16, 32 and 64
+    tokens per wavefront; with H = 1024 split-k, then the LDS-staged kernel; H = 192
+    (H % 128 != 0) runs one k chain in every per-wavefront variant."""
+    rng = np.random.default_rng(H)
+    E, k = 64, 4
+    x = moegen.round_bf16(rng.standard_normal((max(sizes), H)).astype(np.float32))
+    w = moegen.round_bf16((rng.standard_normal((E, H)) * 0.04).astype(np.float32))
+    n = min(sizes)
+    moe.set_cu_budget(4)
+    try:
+        ref = None
+        for T in sizes:
+            log(f"[gpu] router batch-size invariance H={H} T={T}")
+            lg, ids, wt = run(x[:T], w, k)
+            got = (lg[:n], ids[:n], wt[:n])
+            if ref is None:
+                ref = got
+            else:
+                for a, b in zip(got, ref):
+                    assert np.array_equal(a.view(np.uint32) if a.dtype == np.float32 else a,
+                                          b.view(np.uint32) if b.dtype == np.float32 else b), (H, T)
+    finally:
+        moe.set_cu_budget(0)
