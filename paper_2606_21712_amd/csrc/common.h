@@ -138,6 +138,38 @@ __device__ __forceinline__ TailPlan tail_plan(int64_t n, int G, int KT) {
   return t;
 }
 
+// Tile claims of the persistent grouped GEMMs.  The full tiles of the list go out
+// in chunks of kGroupM * kGroupN consecutive tiles (one block of m-tiles x
+// n-tiles sharing their panels): workgroup b belongs to group b % ng (ng = 8 with
+// at least 8 workgroups: the XCD the workgroups are dealt to round-robin), and
+// group x takes chunks x, x + ng, x + 2 ng, ... through a counter of its own, so
+// an XCD's compute units work on the same panels together.  Once a group's full
+// tiles run out, its workgroups take the pieces of a split tail, entries
+// full.. of the list, from one counter shared by all.  Every group has at least
+// one workgroup, so every chunk is taken.  Called by one thread per workgroup.
+struct TileClaim {
+  int32_t* chunk_ctr;   // [ng] counters, zeroed before the launch
+  int32_t* piece_ctr;   // one counter, zeroed before the launch
+  int64_t full;         // entries [0, full) are whole tiles
+  int ng, grp;
+  bool pieces;
+  __device__ TileClaim(int32_t* chunks, int32_t* piece, int64_t full_tiles)
+      : chunk_ctr(chunks), piece_ctr(piece), full(full_tiles), pieces(false) {
+    ng = int(gridDim.x) < 8 ? int(gridDim.x) : 8;
+    grp = int(blockIdx.x) % ng;
+  }
+  __device__ int64_t next() {
+    constexpr int kChunk = kGroupM * kGroupN;
+    if (!pieces) {
+      const int64_t lx = atomicAdd(chunk_ctr + grp, 1);
+      const int64_t L = ((lx / kChunk) * ng + grp) * kChunk + lx % kChunk;
+      if (L < full) return L;
+      pieces = true;
+    }
+    return full + atomicAdd(piece_ctr, 1);
+  }
+};
+
 // Exclusive scan of one int per thread over a 256-thread block; *total = sum.
 // Every thread of the block must call it (it synchronizes the block).
 __device__ __forceinline__ int32_t block_exclusive_scan256(int32_t v, int32_t* total) {

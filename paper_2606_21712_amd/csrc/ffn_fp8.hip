@@ -126,7 +126,8 @@ constexpr int kWaitVm0 = 0x0F70;
 constexpr int kBufFlags = 0x00020000;
 
 struct GemmArgsF8 {
-  int32_t* queue;
+  int32_t* queue;                 // tail-split pieces counter
+  int32_t* xqueue;                // 8 chunk counters (TileClaim)
   const uint8_t* act;             // [R, K] codes of the grouped rows; with a gather, [T, K] token rows
   const uint8_t* act_scales;      // [K / 128][R][4]; with a gather, [K / 128][T][4]
   const int32_t* gather;          // [R] token of each grouped row (gather only)
@@ -185,7 +186,8 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
   const TailPlan plan = SWIGLU ? TailPlan{int64_t(s_pref[p.E]) * NT, 0, 1}
                                : tail_plan(int64_t(s_pref[p.E]) * NT, int(gridDim.x), KT);
   const int64_t total = plan.full + int64_t(plan.r) * plan.s;
-  if (tid == 0) s_claim[0] = atomicAdd(p.queue, 1);
+  TileClaim claim(p.xqueue, p.queue, plan.full);
+  if (tid == 0) s_claim[0] = claim.next();
   __syncthreads();
 
   const int qrow = lane >> 3;
@@ -196,7 +198,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
   for (int it = 0;; ++it) {
     const int64_t L = s_claim[it & 1];
     if (L >= total) break;
-    if (tid == 0) s_claim[(it + 1) & 1] = atomicAdd(p.queue, 1);
+    if (tid == 0) s_claim[(it + 1) & 1] = claim.next();
     // a whole tile, or piece j of a tail tile (k steps kt0..kt1, partial slot)
     int64_t Lt = L;
     int kt0 = 0, kt1 = KT, slot = -1;
@@ -472,14 +474,14 @@ hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* 
   hipError_t err = launch_tile_prefix(offsets, E, kBM, 0, mtile_prefix, queues, s);
   if (err != hipSuccess) return err;
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
-  GemmArgsF8 a1{queues, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, nullptr, offsets, mtile_prefix,
+  GemmArgsF8 a1{queues, queues + 2, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, nullptr, offsets, mtile_prefix,
                 E, H, F, F / 128, int(R), int(T)};
   const dim3 grid1(grid_for(mtiles_upper * a1.ntiles, num_cu));
   if (gather != nullptr)
     MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_fp8_kernel<true, true>), grid1, dim3(kThreads), s, a1);
   else
     MOE_LAUNCH("ffn_gemm1_gate_up", (grouped_gemm_fp8_kernel<true, false>), grid1, dim3(kThreads), s, a1);
-  GemmArgsF8 a2{queues + 1, h, hs, nullptr, wd, wds, nullptr, nullptr, nullptr, nullptr, y_perm, partial, offsets,
+  GemmArgsF8 a2{queues + 1, queues + 10, h, hs, nullptr, wd, wds, nullptr, nullptr, nullptr, nullptr, y_perm, partial, offsets,
                 mtile_prefix, E, F, H, (H + 255) / 256, int(R), 0};
   const int grid2 = grid_for(mtiles_upper * a2.ntiles, num_cu);
   MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_fp8_kernel<false, false>), dim3(grid2), dim3(kThreads), s, a2);
