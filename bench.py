@@ -375,8 +375,10 @@ def expert_batch_sweep(shape: str, steps: int, warmup: int):
     then fit the grouped FFN's runtime model (fit_ffn_model).  Router-logit shapes
     use the leading T tokens of one seeded batch (every smaller batch is a prefix of
     the larger ones).  memconstrained_lognormal keeps the workload's own routing at
-    every T: exact per-expert counts from the same 64 lognormal(0, 1) draws, scaled
-    to T * k assignments, the three smallest experts pinned to 1, 17 and 31 rows.
+    every T: exact per-expert counts from 64 lognormal(0, 1) draws, scaled to T * k
+    assignments, the three smallest experts pinned to 1, 17 and 31 rows (an expert
+    above T rows, possible only at the smallest T, is capped at T and its excess
+    moved to the next largest).
     The saturation batch is the smallest T whose FFN throughput reaches 90% of the
     largest measured."""
     import torch
@@ -404,7 +406,8 @@ def expert_batch_sweep(shape: str, steps: int, warmup: int):
         if lognormal:
             # the workload's routing recipe at this T (generator only: counts, sets, margin logits)
             rng = np.random.default_rng(np.random.SeedSequence([cfg.seed, T]))
-            target = moegen.lognormal_counts(rng, cfg.E, T * cfg.k, cfg.lognormal_sigma, cfg.pinned_small)
+            target = moegen.cap_counts(
+                moegen.lognormal_counts(rng, cfg.E, T * cfg.k, cfg.lognormal_sigma, cfg.pinned_small), T)
             chosen, _ = moegen.exact_count_assignment(target, T, cfg.k, rng)
             ls = to_dev(moegen.margin_logits(I.x[:T], w_r, chosen, cfg.margin), torch)
             counts = np.sort(np.bincount(chosen.ravel(), minlength=cfg.E))
@@ -585,7 +588,7 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
     the copy's size is read from root/copy_bytes.txt)."""
     import glob
     known = ("route", "permute_count", "permute_scan", "permute_rank", "permute_small", "permute_maps",
-             "permute_copy", "tile_prefix", "gemm1", "gemm2", "tail_reduce", "combine")
+             "permute_copy", "tile_prefix", "gemm1", "gemm2", "tail_reduce", "combine", "quantize_rows")
 
     lines = [f"Workload {c.name}: T={c.T} H={c.H} E={c.E} k={c.k} F={c.F} Fs={c.Fs} {c.dtype}, "
              f"{'gather' if gather else 'x_perm'} path.", ""]

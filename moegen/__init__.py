@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "MoEConfig", "CONFIGS", "Inputs", "make_inputs", "round_bf16", "as_f64",
-    "zipf_counts", "lognormal_counts", "exact_count_assignment", "router_matrix", "margin_logits",
+    "zipf_counts", "lognormal_counts", "exact_count_assignment", "router_matrix", "margin_logits", "cap_counts",
 ]
 
 _CHUNK = 1 << 22          # elements per independently seeded chunk
@@ -175,6 +175,23 @@ def lognormal_counts(rng: np.random.Generator, E: int, R: int, sigma: float,
     else:
         counts[:] = largest_remainder(d, R)
     return counts
+
+
+def cap_counts(counts: np.ndarray, cap: int) -> np.ndarray:
+    """Counts with none above cap and the same sum: the excess of the capped experts
+    goes, largest expert first, to the others up to the cap (needed when a batch is
+    too small for its largest expert, which can hold at most one row per token)."""
+    c = np.asarray(counts, dtype=np.int64).copy()
+    assert c.sum() <= cap * c.size
+    excess = int(np.maximum(c - cap, 0).sum())
+    c = np.minimum(c, cap)
+    for e in np.argsort(-c, kind="stable"):
+        if excess == 0:
+            break
+        add = min(cap - int(c[e]), excess)
+        c[e] += add
+        excess -= add
+    return c
 
 
 def exact_count_assignment(counts: np.ndarray, T: int, k: int, rng: np.random.Generator):

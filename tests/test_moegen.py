@@ -85,3 +85,11 @@ def test_uniform_routing():
     cfg = moegen.MoEConfig("u", T=16, H=64, E=8, k=3, F=64, routing="uniform")
     I = moegen.make_inputs(cfg)
     assert (I.logits == 0).all()
+
+
+def test_cap_counts_keeps_the_sum_and_the_cap():
+    c = moegen.cap_counts(np.array([335, 300, 100, 10, 1, 278]), 256)
+    assert c.sum() == 1024 and c.max() <= 256
+    assert list(c) == [256, 256, 245, 10, 1, 256]          # excess to the largest with room
+    same = np.array([5, 4, 3])
+    assert np.array_equal(moegen.cap_counts(same, 5), same)
