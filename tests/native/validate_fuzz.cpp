@@ -61,6 +61,7 @@ int main() {
     c = validate_router_topk(pickp(), pickp(), T, E, k, H, int32_t(next() % 3), nullptr, ip,
                              static_cast<const float*>(pickp()));
     c = validate_permute(ip, pickp(), T, E, k, H, dt, ip, ip, ip, ip, pickp(), pickp(), ws);
+    c = validate_permute_static(ip, pickp(), T, E, k, H, dt, ip, ip, ip, ip, pickp());
     c = validate_ffn(pickp(), ip, R, E, H, F, pickp(), pickp(), pickp(), dt, pickp(), pickp(), ws);
     const bool ffn_ok = c.ok();
     c = validate_ffn_gather(pickp(), ip, T, ip, R, E, H, F, pickp(), pickp(), pickp(), dt, pickp(), pickp(), ws);

@@ -79,7 +79,7 @@ def _check_rows(label, rows_tok, rows_r, e_of, xq_host, x_rows_bf16, wg, wu, wd,
     return n_flip
 
 
-@pytest.mark.parametrize("name", ["mixtral4k", "deepseek", "memconstrained"])
+@pytest.mark.parametrize("name", ["mixtral4k", "mixtral32k_zipf", "deepseek", "memconstrained"])
 def test_full_size_layer_mxfp8(name):
     cfg = moegen.CONFIGS[name]
     log(f"[gpu] full-size mxfp8 {name}: generating T={cfg.T} H={cfg.H} E={cfg.E} k={cfg.k} F={cfg.F} Fs={cfg.Fs}")
