@@ -548,6 +548,12 @@ def time_calls(calls, stream, reps: int = 20):
 PMC_PASSES = {
     "sq": "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_WAVE_CYCLES "
           "SQ_WAIT_ANY SQ_WAIT_INST_LDS SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE",
+    "lds": "SQ_LDS_IDX_ACTIVE SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL SQ_INSTS_LDS_LOAD_BANDWIDTH "
+           "SQ_INSTS_LDS_STORE_BANDWIDTH SQ_WAIT_INST_ANY SQ_ACTIVE_INST_MISC SQ_WAVE_CYCLES GRBM_GUI_ACTIVE",
+    "vmem": "SQ_VMEM_TA_ADDR_FIFO_FULL SQ_VMEM_TA_CMD_FIFO_FULL "
+            "SQ_ACTIVE_INST_VMEM SQ_WAVE_CYCLES TA_TA_BUSY TA_ADDR_STALLED_BY_TC_CYCLES TD_TD_BUSY TD_TC_STALL "
+            "TCP_TCC_READ_REQ TCP_TCC_READ_REQ_LATENCY TCP_PENDING_STALL_CYCLES TCP_TCR_TCP_STALL_CYCLES "
+            "GRBM_GUI_ACTIVE",
     "fetch": "FETCH_SIZE GRBM_GUI_ACTIVE",
     "write": "WRITE_SIZE GRBM_GUI_ACTIVE",
 }
@@ -708,6 +714,59 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
                          f"{f(hbm / nbytes if hbm and nbytes else None, '.2f')} | {f(gbs, '.0f')}{mark} | "
                          f"{f(100 * gbs / PEAK_HBM_GBS if gbs else None, '.1f')}{mark} |")
         lines.append("")
+        lds_rows = [lab for lab in per if "SQ_LDS_IDX_ACTIVE" in per[lab] and lab.startswith("gemm")]
+        if lds_rows:
+            lines += ["LDS of the grouped GEMMs (the `lds` pass; per compute unit and elapsed cycle): LDS active = "
+                      "SQ_LDS_IDX_ACTIVE / (cycles x 256 CUs); bytes read by LDS instructions = "
+                      "SQ_INSTS_LDS_LOAD_BANDWIDTH x 64 / (cycles x 256) (the operand fragments; the direct "
+                      "global -> LDS loads that fill the stages are not LDS instructions); data / command FIFO "
+                      "full = SQ_LDS_DATA_FIFO_FULL, SQ_LDS_CMD_FIFO_FULL / (cycles x 256); any-instruction "
+                      "wait and misc (barrier, waitcnt) active = SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_MISC / "
+                      "SQ_WAVE_CYCLES.", "",
+                      "| kernel | LDS active % | LDS-read bytes per CU cycle | LDS-instruction store bytes "
+                      "per CU cycle | data FIFO full % | command FIFO full % | wave-cycles waiting on an "
+                      "instruction % | misc active % |",
+                      "|---|---|---|---|---|---|---|---|"]
+            for lab in sorted(lds_rows):
+                m = {k: float(np.mean(v)) for k, v in per[lab].items()}
+                cu_cyc = m["GRBM_GUI_ACTIVE"] / NUM_XCD * NUM_CU
+                wc = m.get("SQ_WAVE_CYCLES")
+
+                def pct(k, d):
+                    return "-" if k not in m or not d else f"{100 * m[k] / d:.1f}"
+                rd = m.get("SQ_INSTS_LDS_LOAD_BANDWIDTH", 0.0) * 64 / cu_cyc
+                wr = m.get("SQ_INSTS_LDS_STORE_BANDWIDTH", 0.0) * 64 / cu_cyc
+                lines.append(f"| {lab} | {pct('SQ_LDS_IDX_ACTIVE', cu_cyc)} | {rd:.1f} | {wr:.1f} | "
+                             f"{pct('SQ_LDS_DATA_FIFO_FULL', cu_cyc)} | {pct('SQ_LDS_CMD_FIFO_FULL', cu_cyc)} | "
+                             f"{pct('SQ_WAIT_INST_ANY', wc)} | {pct('SQ_ACTIVE_INST_MISC', wc)} |")
+            lines.append("")
+        vm_rows = [lab for lab in per if "TA_TA_BUSY" in per[lab] and lab.startswith("gemm")]
+        if vm_rows:
+            lines += ["Load path of the grouped GEMMs (the `vmem` pass): TA / TD busy and stalled = TA_TA_BUSY, "
+                      "TA_ADDR_STALLED_BY_TC_CYCLES, TD_TD_BUSY, TD_TC_STALL / (cycles x 256 CUs); "
+                      "L1 -> L2 read latency = "
+                      "TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ; TA FIFO full = SQ_VMEM_TA_ADDR_FIFO_FULL + "
+                      "SQ_VMEM_TA_CMD_FIFO_FULL / (cycles x 256); TCP pending / TCR stall = "
+                      "TCP_PENDING_STALL_CYCLES, TCP_TCR_TCP_STALL_CYCLES / (cycles x 256).", "",
+                      "| kernel | TA busy % | TA stalled by L2 % | TD busy % | TD stalled by L2 % | "
+                      "L1 -> L2 read latency, cycles | TA FIFO full % | "
+                      "TCP pending stall % | TCR stall % |",
+                      "|---|---|---|---|---|---|---|---|---|"]
+            for lab in sorted(vm_rows):
+                m = {k: float(np.mean(v)) for k, v in per[lab].items()}
+                cu_cyc = m["GRBM_GUI_ACTIVE"] / NUM_XCD * NUM_CU
+
+                def pc(*ks):
+                    return "-" if any(k not in m for k in ks) else f"{100 * sum(m[k] for k in ks) / cu_cyc:.1f}"
+
+                def ratio(a, b):
+                    return "-" if not m.get(b) or a not in m else f"{m[a] / m[b]:.0f}"
+                lines.append(f"| {lab} | {pc('TA_TA_BUSY')} | {pc('TA_ADDR_STALLED_BY_TC_CYCLES')} | "
+                             f"{pc('TD_TD_BUSY')} | {pc('TD_TC_STALL')} | "
+                             f"{ratio('TCP_TCC_READ_REQ_LATENCY', 'TCP_TCC_READ_REQ')} | "
+                             f"{pc('SQ_VMEM_TA_ADDR_FIFO_FULL', 'SQ_VMEM_TA_CMD_FIFO_FULL')} | "
+                             f"{pc('TCP_PENDING_STALL_CYCLES')} | {pc('TCP_TCR_TCP_STALL_CYCLES')} |")
+            lines.append("")
         g = per.get("gemm1")
         if g and "FETCH_SIZE" in g and "WRITE_SIZE" in g and factor:
             hbm = float(np.mean(g["FETCH_SIZE"])) * 1024 * factor["FETCH_SIZE"] + \
