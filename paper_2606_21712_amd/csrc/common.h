@@ -138,35 +138,47 @@ __device__ __forceinline__ TailPlan tail_plan(int64_t n, int G, int KT) {
   return t;
 }
 
-// Tile claims of the persistent grouped GEMMs.  The full tiles of the list go out
-// in chunks of kGroupM * kGroupN consecutive tiles (one block of m-tiles x
-// n-tiles sharing their panels): workgroup b belongs to group b % ng (ng = 8 with
-// at least 8 workgroups: the XCD the workgroups are dealt to round-robin), and
-// group x takes chunks x, x + ng, x + 2 ng, ... through a counter of its own, so
-// an XCD's compute units work on the same panels together.  Once a group's full
-// tiles run out, its workgroups take the pieces of a split tail, entries
-// full.. of the list, from one counter shared by all.  Every group has at least
-// one workgroup, so every chunk is taken.  Called by one thread per workgroup.
+// Tile claims of the persistent grouped GEMMs.  Workgroup b belongs to group
+// b % ng (ng = 8 with at least 8 workgroups: the XCD the workgroups are dealt to
+// round-robin).  When the experts hold at least two m-tiles each on average, the
+// leading full tiles of the list go out in chunks of kGroupM * kGroupN
+// consecutive tiles (one block of m-tiles x n-tiles sharing their panels), as
+// many chunks as make the same whole number per group: group x takes chunks x,
+// x + ng, x + 2 ng, ... through a counter of its own, so an XCD's compute units
+// work on the same panels together.  The rest of the full tiles (fewer than ng
+// chunks' worth), then the pieces of a split tail (entries full..), go out one at
+// a time from a counter shared by all, so no XCD idles while another still holds
+// tiles.  Every group has at least one workgroup, so every chunk is taken.  With
+// no chunk to hand out the first claim goes straight to the shared counter: the
+// counters are device-scope atomics that serialize, and in a launch of one tile
+// per workgroup a second dependent atomic before the first tile delays the last
+// workgroup's start.  With about one m-tile per expert a chunk shares no weight
+// panel, and a single queue measured faster.  Called by one thread per workgroup.
 struct TileClaim {
+  static constexpr int kChunk = kGroupM * kGroupN;
   int32_t* chunk_ctr;   // [ng] counters, zeroed before the launch
-  int32_t* piece_ctr;   // one counter, zeroed before the launch
-  int64_t full;         // entries [0, full) are whole tiles
+  int32_t* shared_ctr;  // one counter, zeroed before the launch
+  int64_t chunked;      // entries [0, chunked) go out in chunks
   int ng, grp;
-  bool pieces;
-  __device__ TileClaim(int32_t* chunks, int32_t* piece, int64_t full_tiles)
-      : chunk_ctr(chunks), piece_ctr(piece), full(full_tiles), pieces(false) {
+  bool in_shared;
+  // full_tiles: entries [0, full_tiles) are whole tiles; mtiles, E: the m-tiles of
+  // all experts and the number of experts.
+  __device__ TileClaim(int32_t* chunks, int32_t* shared, int64_t full_tiles, int mtiles, int E)
+      : chunk_ctr(chunks), shared_ctr(shared) {
     ng = int(gridDim.x) < 8 ? int(gridDim.x) : 8;
     grp = int(blockIdx.x) % ng;
+    const int64_t per = int64_t(kChunk) * ng;
+    chunked = mtiles >= 2 * E ? full_tiles / per * per : 0;
+    in_shared = chunked == 0;
   }
   __device__ int64_t next() {
-    constexpr int kChunk = kGroupM * kGroupN;
-    if (!pieces) {
+    if (!in_shared) {
       const int64_t lx = atomicAdd(chunk_ctr + grp, 1);
       const int64_t L = ((lx / kChunk) * ng + grp) * kChunk + lx % kChunk;
-      if (L < full) return L;
-      pieces = true;
+      if (L < chunked) return L;
+      in_shared = true;
     }
-    return full + atomicAdd(piece_ctr, 1);
+    return chunked + atomicAdd(shared_ctr, 1);
   }
 };
 

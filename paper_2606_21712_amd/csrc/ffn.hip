@@ -15,8 +15,11 @@
 // claim such chunks of 32 tiles from a counter of their own, every eighth chunk
 // of the list, so the 32 compute units of an XCD work on the same panels at the
 // same time and share its L2; inside an XCD cheap and costly tiles balance
-// dynamically.  (Measured against one queue over the whole list, same inputs:
-// GEMM-1 -1% to -4%, GEMM-2 -4% to -7% on the four bf16 workloads.)
+// dynamically.  Only as many chunks as give every XCD the same number go out
+// this way; the remaining tiles (and a split tail's pieces) come from one
+// shared counter, so a small problem never leaves an XCD idle while another
+// holds whole chunks.  (Measured against one queue over the whole list, same
+// inputs: GEMM-1 -1% to -4%, GEMM-2 -4% to -7% on the four bf16 workloads.)
 //
 // bf16 tile: 256 rows (an expert's last m-tile up to 320) x 256 weight rows x
 // 64 k per step, 8 wavefronts (2 x 4, two per SIMD so one issues MFMAs while
@@ -86,7 +89,7 @@ static_assert(8 * kEpiBytes <= kStageBytes, "epilogue staging fits one stage");
 static_assert(kBM == kTileRows && kBN == kTileCols, "tile shape");
 
 struct GemmArgs {
-  int32_t* queue;                 // tile counter (tail-split pieces), zeroed by tile_prefix_kernel
+  int32_t* queue;                 // shared tile counter (TileClaim), zeroed by tile_prefix_kernel
   int32_t* xqueue;                // kGroups chunk counters (TileClaim), zeroed likewise
   const uint16_t* act;            // [R, K]; with a gather, the token rows [T, K]
   const int32_t* gather;          // [R] token of each grouped row (gather only)
@@ -165,8 +168,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
   const TailPlan plan = SWIGLU ? TailPlan{int64_t(s_pref[p.E]) * NT, 0, 1}
                                : tail_plan(int64_t(s_pref[p.E]) * NT, int(gridDim.x), KT);
   const int64_t total = plan.full + int64_t(plan.r) * plan.s;
-  // Tiles in chunks per XCD, the tail's pieces from one shared counter (TileClaim).
-  TileClaim claim(p.xqueue, p.queue, plan.full);
+  // Tiles in chunks per XCD, the rest and the tail's pieces from one shared counter (TileClaim).
+  TileClaim claim(p.xqueue, p.queue, plan.full, s_pref[p.E], p.E);
   if (tid == 0) s_claim[0] = claim.next();
   __syncthreads();
 

@@ -126,7 +126,7 @@ constexpr int kWaitVm0 = 0x0F70;
 constexpr int kBufFlags = 0x00020000;
 
 struct GemmArgsF8 {
-  int32_t* queue;                 // tail-split pieces counter
+  int32_t* queue;                 // shared tile counter (TileClaim)
   int32_t* xqueue;                // 8 chunk counters (TileClaim)
   const uint8_t* act;             // [R, K] codes of the grouped rows; with a gather, [T, K] token rows
   const uint8_t* act_scales;      // [K / 128][R][4]; with a gather, [K / 128][T][4]
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
   const TailPlan plan = SWIGLU ? TailPlan{int64_t(s_pref[p.E]) * NT, 0, 1}
                                : tail_plan(int64_t(s_pref[p.E]) * NT, int(gridDim.x), KT);
   const int64_t total = plan.full + int64_t(plan.r) * plan.s;
-  TileClaim claim(p.xqueue, p.queue, plan.full);
+  TileClaim claim(p.xqueue, p.queue, plan.full, s_pref[p.E], p.E);
   if (tid == 0) s_claim[0] = claim.next();
   __syncthreads();
 
