@@ -161,6 +161,105 @@ def copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes": nbytes, "ms": ms, "GBps_read_plus_write": 2 * nbytes / ms / 1e6}))
 
 
+def dense_ceiling(cname: str, reps: int = 5):
+    """The vendor GEMM on the same work, for context: torch.matmul (hipBLASLt) run
+    expert by expert over the workload's own group sizes (the routing and grouping
+    of this library's route and permute on the workload's logits), bf16 in, fp32
+    accumulation, bf16 out, with contiguous pre-transposed weights and the rows of
+    each group contiguous (x_perm), so the library gets its easiest layout.  Both
+    projections are timed (the gate and up weights as one [H, 2F] matrix per expert;
+    the down projection on a random h), without the SwiGLU between them; then one
+    dense GEMM of each projection's total size (M = R) as an upper bound.  Weights and
+    h are random normal with the workload's scale (the values only matter for the
+    board's power draw).  Median over reps of the whole loop, HIP events."""
+    import torch
+
+    import moegen
+    import paper_2606_21712_amd as moe
+
+    c = moegen.CONFIGS[cname]
+    assert c.dtype == "bf16", "bf16 workloads only"
+    T, H, E, k, F, R = c.T, c.H, c.E, c.k, c.F, c.R
+    log(f"dense ceiling {cname}: generating T={T} H={H} E={E} k={k} F={F}")
+    I = moegen.make_inputs(c, with_weights=False)
+    x, logits = to_dev(I.x, torch), to_dev(I.logits, torch)
+    ids = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    moe.moe_route(logits, k, c.renormalize, ids, w)
+    perm = moe.moe_permute(ids, x, E)
+    torch.cuda.synchronize()
+    offs = perm["offsets"].cpu().tolist()
+    x_perm = perm["x_perm"]
+    g = torch.Generator(device="cuda").manual_seed(c.seed)
+    w_gu = (torch.randn((E, H, 2 * F), generator=g, device="cuda") / H ** 0.5).to(torch.bfloat16)
+    w_d = (torch.randn((E, F, H), generator=g, device="cuda") / F ** 0.5).to(torch.bfloat16)
+    h = torch.randn((R, F), generator=g, device="cuda").to(torch.bfloat16)
+    gu = torch.empty((R, 2 * F), dtype=torch.bfloat16, device="cuda")
+    y = torch.empty((R, H), dtype=torch.bfloat16, device="cuda")
+    groups = [(e, offs[e], offs[e + 1]) for e in range(E) if offs[e + 1] > offs[e]]
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    def gate_up():
+        for e, a, b in groups:
+            torch.matmul(x_perm[a:b], w_gu[e], out=gu[a:b])
+
+    def down():
+        for e, a, b in groups:
+            torch.matmul(h[a:b], w_d[e], out=y[a:b])
+
+    t1, t2 = timed(gate_up), timed(down)
+    t1d = timed(lambda: torch.matmul(x_perm, w_gu[0], out=gu))
+    t2d = timed(lambda: torch.matmul(h, w_d[0], out=y))
+    del w_gu, w_d, h, gu
+    # this library's grouped FFN (gather path) on the same routing, in the same process
+    wg = (torch.randn((E, F, H), generator=g, device="cuda") / H ** 0.5).to(torch.bfloat16)
+    wu = (torch.randn((E, F, H), generator=g, device="cuda") / H ** 0.5).to(torch.bfloat16)
+    wd = (torch.randn((E, H, F), generator=g, device="cuda") / F ** 0.5).to(torch.bfloat16)
+    ws = torch.empty(moe.moe_grouped_ffn_workspace_bytes(R, E, H, F, torch.bfloat16), dtype=torch.uint8,
+                     device="cuda")
+
+    def ours():
+        moe.moe_grouped_ffn_gather(x, perm["sorted_token_ids"], perm["offsets"], wg, wu, wd, y_perm=y, ws=ws)
+
+    ours()
+    torch.cuda.synchronize()
+    moe.profiler_start(reps * 8 + 8)
+    for _ in range(reps):
+        ours()
+    torch.cuda.synchronize()
+    moe.profiler_stop()
+    rec = {}
+    for n, ms in moe.profiler_records():
+        rec.setdefault(n, []).append(ms)
+    o1 = float(np.median(rec["ffn_gemm1_gate_up"]))
+    o2 = float(np.median(rec["ffn_gemm2_down"])) + float(np.median(rec.get("ffn_tail_reduce", [0.0])))
+    f1, f2 = 4.0 * H * F * R, 2.0 * H * F * R
+    print(json.dumps({"dense_ceiling": cname, "library": "torch.matmul (hipBLASLt), bf16",
+                      "experts_run": len(groups), "reps": reps,
+                      "this_library": {"gate_up_swiglu_gather_ms": round(o1, 3),
+                                       "gate_up_tflops": round(f1 / o1 / 1e9, 1),
+                                       "down_ms": round(o2, 3), "down_tflops": round(f2 / o2 / 1e9, 1),
+                                       "ffn_tflops": round((f1 + f2) / (o1 + o2) / 1e9, 1)},
+                      "per_expert": {"gate_up_ms": round(t1, 3), "gate_up_tflops": round(f1 / t1 / 1e9, 1),
+                                     "down_ms": round(t2, 3), "down_tflops": round(f2 / t2 / 1e9, 1),
+                                     "ffn_tflops": round((f1 + f2) / (t1 + t2) / 1e9, 1)},
+                      "one_dense_gemm": {"gate_up_ms": round(t1d, 3), "gate_up_tflops": round(f1 / t1d / 1e9, 1),
+                                         "down_ms": round(t2d, 3), "down_tflops": round(f2 / t2d / 1e9, 1)}}),
+          flush=True)
+
+
 def stream_copy_gbps(nbytes: int = 1 << 30, reps: int = 5) -> float:
     """Practical HBM rate on this GPU: read + write bytes of a plain device copy of
     nbytes (torch's copy kernel), median of reps, run outside any timed region."""
@@ -836,6 +935,8 @@ def main():
                          "counter passes of --profile-run / default runs of --config)")
     ap.add_argument("--probe", action="store_true",
                     help="with --summarize: counters per kernel instantiation of a --route-probe run")
+    ap.add_argument("--dense-ceiling", action="store_true",
+                    help="time torch.matmul (hipBLASLt) expert by expert on the workload's groups, for context")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (HBM counter calibration)")
     ap.add_argument("--sweep", choices=sorted(SWEEP_SHAPES), default=None,
@@ -854,6 +955,8 @@ def main():
                          gather=not args.no_gather)
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.dense_ceiling:
+        return dense_ceiling(args.config)
     if args.route_probe:
         return route_probe()
     if args.router_probe:
