@@ -260,6 +260,109 @@ def dense_ceiling(cname: str, reps: int = 5):
           flush=True)
 
 
+def dense_ceiling_fp8(cname: str, reps: int = 5):
+    """The MXFP8 counterpart of dense_ceiling: this library's MXFP8 grouped FFN
+    (gather path; the token rows quantized once, not timed here) beside the vendor
+    fp8 GEMM, torch._scaled_mm (hipBLASLt) with OCP E4M3 operands and one fp32 scale
+    per tensor (a coarser scaling than MX blocks, so a generous ceiling), expert by
+    expert over the same groups and as one dense GEMM of each projection's total
+    size.  Operands are random normal at the workload's scale."""
+    import torch
+
+    import moegen
+    import paper_2606_21712_amd as moe
+
+    c = moegen.CONFIGS[cname]
+    T, H, E, k, F, R = c.T, c.H, c.E, c.k, c.F, c.R
+    log(f"fp8 dense ceiling {cname}: generating T={T} H={H} E={E} k={k} F={F}")
+    I = moegen.make_inputs(c, with_weights=False)
+    x, logits = to_dev(I.x, torch), to_dev(I.logits, torch)
+    ids = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    moe.moe_route(logits, k, c.renormalize, ids, w)
+    perm = moe.moe_permute(ids, x, E)
+    torch.cuda.synchronize()
+    offs = perm["offsets"].cpu().tolist()
+    groups = [(e, offs[e], offs[e + 1]) for e in range(E) if offs[e + 1] > offs[e]]
+    g = torch.Generator(device="cuda").manual_seed(c.seed)
+
+    def rnd(shape, std):
+        return (torch.randn(shape, generator=g, device="cuda") * std).to(torch.bfloat16)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    f1, f2 = 4.0 * H * F * R, 2.0 * H * F * R
+    out = {"dense_ceiling_fp8": cname, "experts_run": len(groups), "reps": reps}
+    # this library
+    wq_g = moe.quantize_weights_mxfp8(rnd((E, F, H), H ** -0.5))
+    wq_u = moe.quantize_weights_mxfp8(rnd((E, F, H), H ** -0.5))
+    wq_d = moe.quantize_weights_mxfp8(rnd((E, H, F), F ** -0.5))
+    xq = moe.moe_quantize_mxfp8(x)
+    y = torch.empty((R, H), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(moe.moe_grouped_ffn_mxfp8_workspace_bytes(R, E, H, F), dtype=torch.uint8, device="cuda")
+
+    def ours():
+        moe.moe_grouped_ffn_mxfp8_gather(xq, perm["sorted_token_ids"], perm["offsets"], wq_g, wq_u, wq_d,
+                                         y_perm=y, ws=ws)
+
+    ours()
+    torch.cuda.synchronize()
+    moe.profiler_start(reps * 8 + 8)
+    for _ in range(reps):
+        ours()
+    torch.cuda.synchronize()
+    moe.profiler_stop()
+    rec = {}
+    for n, ms in moe.profiler_records():
+        rec.setdefault(n, []).append(ms)
+    o1 = float(np.median(rec["ffn_gemm1_gate_up"]))
+    o2 = float(np.median(rec["ffn_gemm2_down"])) + float(np.median(rec.get("ffn_tail_reduce", [0.0])))
+    out["this_library_mxfp8"] = {"gate_up_swiglu_gather_ms": round(o1, 3), "gate_up_tflops": round(f1 / o1 / 1e9, 1),
+                                 "down_ms": round(o2, 3), "down_tflops": round(f2 / o2 / 1e9, 1),
+                                 "ffn_tflops": round((f1 + f2) / (o1 + o2) / 1e9, 1)}
+    del wq_g, wq_u, wq_d, xq, ws
+    # the vendor GEMM: A row-major [M, K], B column-major [K, N] (the weights' own K-contiguous rows)
+    f8 = torch.float8_e4m3fn
+    one = torch.ones((), dtype=torch.float32, device="cuda")
+    a1 = perm["x_perm"].to(f8)
+    w1 = rnd((E, 2 * F, H), H ** -0.5).to(f8)
+    a2 = rnd((R, F), 1.0).to(f8)
+    w2 = rnd((E, H, F), F ** -0.5).to(f8)
+    gu = torch.empty((R, 2 * F), dtype=torch.bfloat16, device="cuda")
+    try:
+        def gate_up():
+            for e, a, b in groups:
+                gu[a:b] = torch._scaled_mm(a1[a:b], w1[e].t(), scale_a=one, scale_b=one, out_dtype=torch.bfloat16)
+
+        def down():
+            for e, a, b in groups:
+                y[a:b] = torch._scaled_mm(a2[a:b], w2[e].t(), scale_a=one, scale_b=one, out_dtype=torch.bfloat16)
+
+        t1, t2 = timed(gate_up), timed(down)
+        t1d = timed(lambda: torch._scaled_mm(a1, w1[0].t(), scale_a=one, scale_b=one, out_dtype=torch.bfloat16))
+        t2d = timed(lambda: torch._scaled_mm(a2, w2[0].t(), scale_a=one, scale_b=one, out_dtype=torch.bfloat16))
+        out["library"] = "torch._scaled_mm (hipBLASLt), E4M3, per-tensor scales"
+        out["per_expert"] = {"gate_up_ms": round(t1, 3), "gate_up_tflops": round(f1 / t1 / 1e9, 1),
+                             "down_ms": round(t2, 3), "down_tflops": round(f2 / t2 / 1e9, 1),
+                             "ffn_tflops": round((f1 + f2) / (t1 + t2) / 1e9, 1)}
+        out["one_dense_gemm"] = {"gate_up_ms": round(t1d, 3), "gate_up_tflops": round(f1 / t1d / 1e9, 1),
+                                 "down_ms": round(t2d, 3), "down_tflops": round(f2 / t2d / 1e9, 1)}
+    except (RuntimeError, TypeError) as err:
+        out["library_error"] = str(err)[:300]
+    print(json.dumps(out), flush=True)
+
+
 def stream_copy_gbps(nbytes: int = 1 << 30, reps: int = 5) -> float:
     """Practical HBM rate on this GPU: read + write bytes of a plain device copy of
     nbytes (torch's copy kernel), median of reps, run outside any timed region."""
@@ -956,7 +1059,7 @@ def main():
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
     if args.dense_ceiling:
-        return dense_ceiling(args.config)
+        return dense_ceiling_fp8(args.config) if args.mxfp8 else dense_ceiling(args.config)
     if args.route_probe:
         return route_probe()
     if args.router_probe:
