@@ -756,6 +756,7 @@ PMC_PASSES = {
             "SQ_ACTIVE_INST_VMEM SQ_WAVE_CYCLES TA_TA_BUSY TA_ADDR_STALLED_BY_TC_CYCLES TD_TD_BUSY TD_TC_STALL "
             "TCP_TCC_READ_REQ TCP_TCC_READ_REQ_LATENCY TCP_PENDING_STALL_CYCLES TCP_TCR_TCP_STALL_CYCLES "
             "GRBM_GUI_ACTIVE",
+    "l2": "TCC_HIT TCC_MISS TCC_EA0_RDREQ TCC_EA0_RDREQ_LEVEL GRBM_GUI_ACTIVE",
     "fetch": "FETCH_SIZE GRBM_GUI_ACTIVE",
     "write": "WRITE_SIZE GRBM_GUI_ACTIVE",
 }
@@ -968,6 +969,25 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
                              f"{ratio('TCP_TCC_READ_REQ_LATENCY', 'TCP_TCC_READ_REQ')} | "
                              f"{pc('SQ_VMEM_TA_ADDR_FIFO_FULL', 'SQ_VMEM_TA_CMD_FIFO_FULL')} | "
                              f"{pc('TCP_PENDING_STALL_CYCLES')} | {pc('TCP_TCR_TCP_STALL_CYCLES')} |")
+            lines.append("")
+        l2_rows = [lab for lab in per if "TCC_HIT" in per[lab] and "TCC_MISS" in per[lab]]
+        if l2_rows:
+            lines += ["L2 (the `l2` pass): hit rate = TCC_HIT / (TCC_HIT + TCC_MISS) over all requests reaching "
+                      "the L2s; reads sent past the L2 (to the Infinity Cache or HBM) per algorithmic byte = "
+                      "TCC_EA0_RDREQ x 128 B / algorithmic bytes (requests of up to 128 B); their mean time in "
+                      "flight = TCC_EA0_RDREQ_LEVEL / TCC_EA0_RDREQ (cycles, Little's law).", "",
+                      "| kernel | L2 hit rate % | read requests past L2 x 128 B / algorithmic bytes | "
+                      "mean read time past L2, cycles |",
+                      "|---|---|---|---|"]
+            for lab in sorted(l2_rows, key=lambda l: -float(np.mean(per[l]["us"]))):
+                m = {k: float(np.mean(v)) for k, v in per[lab].items()}
+                tot = m["TCC_HIT"] + m["TCC_MISS"]
+                _, nbytes = algorithmic_work(c, lab, gather)
+                rd = m.get("TCC_EA0_RDREQ")
+                past = f"{rd * 128 / nbytes:.2f}" if rd and nbytes else "-"
+                lat = f"{m['TCC_EA0_RDREQ_LEVEL'] / rd:.0f}" if rd and "TCC_EA0_RDREQ_LEVEL" in m else "-"
+                lines.append(f"| {lab} | {100 * m['TCC_HIT'] / tot:.1f} | {past} | {lat} |" if tot else
+                             f"| {lab} | - | {past} | {lat} |")
             lines.append("")
         g = per.get("gemm1")
         if g and "FETCH_SIZE" in g and "WRITE_SIZE" in g and factor:
