@@ -428,7 +428,7 @@ def route_probe(reps: int = 10):
 PEAK_FP8_TFLOPS = 5000.0        # MI355X dense fp8 MFMA
 
 
-def mxfp8_bench(config: str, steps: int, warmup: int):
+def mxfp8_bench(config: str, steps: int, warmup: int, profile_run: bool = False):
     """The layer with MXFP8 expert GEMMs on one workload: one JSON line (a separate
     measurement; the bf16 line is the headline).  Weights are quantized once, outside
     the timed region; inside it every step routes, permutes, quantizes x, runs both
@@ -449,6 +449,15 @@ def mxfp8_bench(config: str, steps: int, warmup: int):
 
     def step():
         layer.run(x, logits, *wq, *wqs, renormalize=c.renormalize, stream=stream)
+
+    if profile_run:
+        # what the counter passes see: one warmup step, then two steps
+        for i in range(3):
+            log(f"mxfp8 profile run: layer step {i + 1} of 3")
+            step()
+            torch.cuda.synchronize()
+        print(json.dumps({"profile_run": c.name, "mxfp8": True, "steps": 3}), flush=True)
+        return
 
     for _ in range(warmup):
         step()
@@ -663,12 +672,28 @@ def expert_batch_sweep(shape: str, steps: int, warmup: int):
 
 
 # --------------------------------------------------------------------------- algorithmic work per kernel
-def algorithmic_work(c, role: str, gather: bool = True):
+def algorithmic_work(c, role: str, gather: bool = True, mx: bool = False):
     """(flops, bytes) one launch of a kernel of the layer must do at the least on
     workload c: every operand read once, every result written once, no padding.
-    role is a kernel label from kernel_label() (".shared" for the shared expert)."""
+    role is a kernel label from kernel_label() (".shared" for the shared expert).
+    mx: the MXFP8 layer (GEMM operands as one-byte codes plus a one-byte scale per
+    32 along k; x, y and y_perm stay bf16)."""
     b = 4 if c.dtype == "f32" else 2
     T, H, E, k, F, Fs, R = c.T, c.H, c.E, c.k, c.F, c.Fs, c.R
+    if mx:
+        q = 1 + 1 / 32                                   # bytes per element: code + its share of a scale
+        base = role.split(".")[0]
+        shared = role.endswith(".shared")
+        if base == "quantize_rows":
+            return 0.0, T * H * 2 + T * H * q
+        if base == "gemm1":
+            if shared:
+                return 4.0 * H * Fs * T, 2 * Fs * H * q + T * H * q + T * Fs * q
+            return 4.0 * H * F * R, 2 * E * F * H * q + T * H * q + R * 4 + R * F * q
+        if base == "gemm2":
+            if shared:
+                return 2.0 * H * Fs * T, Fs * H * q + T * Fs * q + T * H * 2
+            return 2.0 * H * F * R, E * H * F * q + R * F * q + R * H * 2
     units = (R + 1023) // 1024
     shared = role.endswith(".shared")
     base = role.split(".")[0]
@@ -750,6 +775,8 @@ def time_calls(calls, stream, reps: int = 20):
 PMC_PASSES = {
     "sq": "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_WAVE_CYCLES "
           "SQ_WAIT_ANY SQ_WAIT_INST_LDS SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE",
+    "sq8": "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_INSTS_VALU_MFMA_MOPS_F8 SQ_INSTS_VALU_MFMA_MOPS_F6F4 "
+           "SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_LDS SQ_INSTS_LDS GRBM_GUI_ACTIVE",
     "lds": "SQ_LDS_IDX_ACTIVE SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL SQ_INSTS_LDS_LOAD_BANDWIDTH "
            "SQ_INSTS_LDS_STORE_BANDWIDTH SQ_WAIT_INST_ANY SQ_ACTIVE_INST_MISC SQ_WAVE_CYCLES GRBM_GUI_ACTIVE",
     "vmem": "SQ_VMEM_TA_ADDR_FIFO_FULL SQ_VMEM_TA_CMD_FIFO_FULL "
@@ -789,7 +816,7 @@ def _segments(dispatches):
     return out
 
 
-def summarize(root, c, warmup: int, steps: int, gather: bool = True):
+def summarize(root, c, warmup: int, steps: int, gather: bool = True, mx: bool = False):
     """Markdown tables from the rocprofv3 output under root:
     root/trace/*kernel_trace.csv (a default bench.py run: warmup, then the timed
     steps), root/<pass>/*counter_collection.csv (--profile-run under --pmc), and
@@ -874,8 +901,9 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
                       "kernels' counters below.", ""]
         lines += ["Columns: duration under the counter passes; shader clock = GRBM_GUI_ACTIVE per XCD / "
                   "duration (kernels of 100 us or more); MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x "
-                  "1024 SIMDs); MFMA-work cycles = counted bf16 flop (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) / "
-                  "(256 CUs x 4096 flop per cycle), over the elapsed cycles; waiting = SQ_WAIT_ANY / "
+                  "1024 SIMDs); MFMA-work cycles = counted MFMA flop (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 at 4096 flop "
+                  "per CU cycle, SQ_INSTS_VALU_MFMA_MOPS_F8 + _F6F4 x 512 at 8192) / 256 CUs, over the elapsed "
+                  "cycles; waiting = SQ_WAIT_ANY / "
                   "SQ_WAVE_CYCLES, LDS-issue wait = SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES; bytes = FETCH_SIZE + "
                   "WRITE_SIZE (bytes leaving or entering the L2s: Infinity Cache hits included), calibrated; "
                   "GB/s = algorithmic bytes / the traced average duration (* : kernel not in the timed "
@@ -895,9 +923,12 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
             clk = cyc / (us * 1e3) if cyc and us >= 100 else None
             busy = 100 * m["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * NUM_SIMD) \
                 if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in m else None
-            flops, nbytes = algorithmic_work(c, lab, gather)
-            cflop = m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
-            work = cflop / (NUM_CU * BF16_FLOP_PER_CU_CLK) / cyc if cyc and cflop else None
+            flops, nbytes = algorithmic_work(c, lab, gather, mx)
+            cflop16 = m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
+            cflop8 = (m.get("SQ_INSTS_VALU_MFMA_MOPS_F8", 0.0) + m.get("SQ_INSTS_VALU_MFMA_MOPS_F6F4", 0.0)) * 512
+            cflop = cflop16 + cflop8
+            work = (cflop16 / BF16_FLOP_PER_CU_CLK + cflop8 / (2 * BF16_FLOP_PER_CU_CLK)) / NUM_CU / cyc \
+                if cyc and cflop else None
             wait = 100 * m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"] \
                 if m.get("SQ_WAVE_CYCLES") and "SQ_WAIT_ANY" in m else None
             lwait = 100 * m["SQ_WAIT_INST_LDS"] / m["SQ_WAVE_CYCLES"] \
@@ -982,7 +1013,7 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True):
             for lab in sorted(l2_rows, key=lambda l: -float(np.mean(per[l]["us"]))):
                 m = {k: float(np.mean(v)) for k, v in per[lab].items()}
                 tot = m["TCC_HIT"] + m["TCC_MISS"]
-                _, nbytes = algorithmic_work(c, lab, gather)
+                _, nbytes = algorithmic_work(c, lab, gather, mx)
                 rd = m.get("TCC_EA0_RDREQ")
                 past = f"{rd * 128 / nbytes:.2f}" if rd and nbytes else "-"
                 lat = f"{m['TCC_EA0_RDREQ_LEVEL'] / rd:.0f}" if rd and "TCC_EA0_RDREQ_LEVEL" in m else "-"
@@ -1075,7 +1106,7 @@ def main():
         return summarize_probe(args.summarize)
     if args.summarize:
         return summarize(args.summarize, moegen.CONFIGS[args.config], args.warmup, args.steps,
-                         gather=not args.no_gather)
+                         gather=not args.no_gather, mx=args.mxfp8)
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
     if args.dense_ceiling:
@@ -1085,7 +1116,7 @@ def main():
     if args.router_probe:
         return router_probe()
     if args.mxfp8:
-        return mxfp8_bench(args.config, args.steps, args.warmup)
+        return mxfp8_bench(args.config, args.steps, args.warmup, profile_run=args.profile_run)
     if args.sweep:
         return expert_batch_sweep(args.sweep, args.steps, args.warmup)
 
