@@ -140,7 +140,27 @@ def cpu_baseline(I, tokens, min_seconds: float = 10.0, max_passes: int = 8):
     return dict(value=passes * len(tokens) / dt, unit="tokens/s", cores=int(threads), kind="oracle",
                 sample=f"{len(tokens)} of {c.T} tokens through the whole layer "
                        f"(fp64 numpy, route + per-expert SwiGLU + combine), {passes} passes, "
-                       f"{dt:.1f} s"), y
+                       f"{dt:.1f} s", blas=_blas_name(), cpu=_cpu_model()), y
+
+
+def _blas_name() -> str:
+    """numpy's BLAS library and version, for the CPU baseline's record."""
+    try:
+        blas = np.show_config(mode="dicts").get("Build Dependencies", {}).get("blas", {})
+        return f"{blas.get('name', '?')} {blas.get('version', '')}".strip()
+    except Exception:                                  # older numpy: no dict mode
+        return "unknown"
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def copy_calibration(nbytes: int):
