@@ -383,6 +383,56 @@ def dense_ceiling_fp8(cname: str, reps: int = 5):
     print(json.dumps(out), flush=True)
 
 
+def mfma_ceiling(reps: int = 3):
+    """What the matrix cores sustain on this board with no memory traffic: the
+    register-only probe of libmoe_probe.so (a measurement tool built beside the
+    library, not part of the MoE path) for bf16 and MX-scaled E4M3 MFMAs, with
+    constant operands and with operands redrawn as they run.  Under the board's
+    power limit the second is the ceiling a GEMM on real data can approach.
+    Median over reps of one launch, HIP events; 2048 workgroups of 4 wavefronts."""
+    import ctypes
+
+    import torch
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_21712_amd", "libmoe_probe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built (run __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    fn = lib.moe_probe_mfma_rate
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    blocks, waves = 2048, 4
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    rows = []
+    for fp8 in (0, 1):
+        iters = 8000 if fp8 else 16000                        # multiples of 4
+        flop_per_mfma = 131072 if fp8 else 32768
+        peak = PEAK_FP8_TFLOPS if fp8 else PEAK_BF16_TFLOPS
+        for rnd in (0, 1):
+            def call():
+                rc = fn(fp8, rnd, blocks, iters, out.data_ptr(), stream.cuda_stream)
+                if rc != 0:
+                    raise RuntimeError(f"moe_probe_mfma_rate returned {rc}")
+            call()
+            torch.cuda.synchronize()
+            assert bool(torch.isfinite(out).all()), "probe accumulators not finite"
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                call()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            ms = float(np.median(ts))
+            tflops = blocks * waves * iters * 8 * flop_per_mfma / (ms * 1e-3) / 1e12
+            rows.append({"mfma": "v_mfma_scale_f32_32x32x64_f8f6f4 (E4M3)" if fp8 else "v_mfma_f32_32x32x16_bf16",
+                         "operands": "redrawn" if rnd else "constant", "ms": round(ms, 3),
+                         "tflops": round(tflops, 1), "frac_of_peak": round(tflops / peak, 4)})
+            log(f"mfma ceiling: {rows[-1]}")
+    print(json.dumps({"mfma_ceiling": rows, "workgroups": blocks, "wavefronts_per_workgroup": waves}), flush=True)
+
+
 def stream_copy_gbps(nbytes: int = 1 << 30, reps: int = 5) -> float:
     """Practical HBM rate on this GPU: read + write bytes of a plain device copy of
     nbytes (torch's copy kernel), median of reps, run outside any timed region."""
@@ -1066,14 +1116,14 @@ def summarize_probe(root):
             d["us"] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
         for d in by_disp.values():
             m = re.search(r"(\w+_kernel<[^()]*>)", d["name"])
-            if not m or not m.group(1).startswith(("route_kernel", "router_")):
+            if not m or not m.group(1).startswith(("route_kernel", "router_", "mfma_rate_kernel")):
                 continue
             slot = per.setdefault(m.group(1), {})
             for k, v in d["counters"].items():
                 slot.setdefault(k, []).append(v)
             slot.setdefault("us", []).append(d["us"])
-    lines = ["| kernel | dispatches | us (pmc run) | VALU instr | VALU issue share % | wave-cycles waiting % | "
-             "FETCH_SIZE KiB | WRITE_SIZE KiB |", "|---|---|---|---|---|---|---|---|"]
+    lines = ["| kernel | dispatches | us (pmc run) | clock GHz | MFMA busy % | VALU instr | VALU issue share % | "
+             "wave-cycles waiting % | FETCH_SIZE KiB | WRITE_SIZE KiB |", "|---|---|---|---|---|---|---|---|---|---|"]
     for name, sl in per.items():
         m = {k: float(np.median(v)) for k, v in sl.items()}
         cyc = m.get("GRBM_GUI_ACTIVE", 0) / NUM_XCD
@@ -1084,7 +1134,11 @@ def summarize_probe(root):
 
         def f(v, fmt):
             return "-" if v is None else format(v, fmt)
-        lines.append(f"| `{name}` | {len(sl['us'])} | {m['us']:.1f} | {f(valu, '.3g')} | {f(share, '.1f')} | "
+        clk = cyc / (m["us"] * 1e3) if cyc and m["us"] >= 100 else None
+        busy = 100 * m["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * NUM_SIMD) if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in m \
+            else None
+        lines.append(f"| `{name}` | {len(sl['us'])} | {m['us']:.1f} | {f(clk, '.3f')} | {f(busy, '.1f')} | "
+                     f"{f(valu, '.3g')} | {f(share, '.1f')} | "
                      f"{f(wait, '.1f')} | {f(m.get('FETCH_SIZE'), '.0f')} | {f(m.get('WRITE_SIZE'), '.0f')} |")
     print("\n".join(lines))
 
@@ -1109,6 +1163,8 @@ def main():
                          "counter passes of --profile-run / default runs of --config)")
     ap.add_argument("--probe", action="store_true",
                     help="with --summarize: counters per kernel instantiation of a --route-probe run")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="the matrix cores' rate with no memory traffic (register-only probe), bf16 and fp8")
     ap.add_argument("--dense-ceiling", action="store_true",
                     help="time torch.matmul (hipBLASLt) expert by expert on the workload's groups, for context")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -1131,6 +1187,8 @@ def main():
         return copy_calibration(args.copy_calibration)
     if args.dense_ceiling:
         return dense_ceiling_fp8(args.config) if args.mxfp8 else dense_ceiling(args.config)
+    if args.mfma_ceiling:
+        return mfma_ceiling()
     if args.route_probe:
         return route_probe()
     if args.router_probe:
