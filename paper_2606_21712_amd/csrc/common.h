@@ -65,7 +65,7 @@ __device__ __forceinline__ int find_expert(const int32_t* pref, int E, int64_t q
 
 // ----------------------------------------------------------------------------- tile list
 // The grouped GEMMs walk one flattened list of output tiles: experts in order,
-// expert e owning pref[e+1] - pref[e] m-tiles of kTileRows rows times NT n-tiles.
+// expert e owning pref[e+1] - pref[e] m-tiles times NT n-tiles.
 // Inside an expert, blocks of up to kGroupM m-tiles are swept in groups of
 // kGroupN n-tiles with the m-tile varying fastest, so the tiles in flight at
 // one time share a few weight and activation panels.
@@ -75,22 +75,17 @@ constexpr int kGroupM = 4;
 struct TileCoord {
   int e;          // expert
   int row0;       // first grouped row of the tile
-  int row_stop;   // end of the tile's rows: row0 + 256, or the expert's end for its last m-tile
+  int row_stop;   // end of the tile's rows
   int nt;         // n-tile index
 };
 
-// m-tiles of an expert with c rows: ceil(c / 256), or with extra > 0 the count
-// that lets the last tile take up to 256 + extra rows.
-__host__ __device__ __forceinline__ int mtiles_of(int c, int extra) {
-  if (c <= 0) return 0;
-  const int rest = c - extra;
-  return rest <= 0 ? 1 : (rest + kTileRows - 1) / kTileRows;
-}
-
 // Tile L of the list; pref/off are the m-tile prefix and row offsets (E + 1
-// entries, typically staged in LDS).  All lanes pass the same L.  The last
-// m-tile of an expert ends at the expert's end (at most 256 + the extra rows
-// the prefix was built with), every other one after 256 rows.
+// entries, typically staged in LDS).  All lanes pass the same L.  BLOCKS (the
+// bf16 GEMMs, prefix of ceil(c / kTileRowsMax) m-tiles): the expert's
+// ceil(c / 32) row blocks are shared out evenly, m-tile mt holding blocks
+// [mt nb / mt_e, (mt + 1) nb / mt_e), at most 10 of them (320 rows).  Otherwise
+// (prefix of ceil(c / kTileRows)): kTileRows rows each, the last one shorter.
+template <bool BLOCKS = false>
 __device__ __forceinline__ TileCoord decode_tile(int64_t L, const int32_t* pref, const int32_t* off, int E,
                                                  int NT) {
   TileCoord t;
@@ -106,9 +101,16 @@ __device__ __forceinline__ TileCoord decode_tile(int64_t L, const int32_t* pref,
   const int rem2 = rem - ng * bm * kGroupN;
   const int mt = mbi * kGroupM + rem2 % bm;
   t.nt = ng * kGroupN + rem2 / bm;
-  t.row0 = __builtin_amdgcn_readfirstlane(off[t.e]) + mt * kTileRows;
+  const int row_beg = __builtin_amdgcn_readfirstlane(off[t.e]);
   const int row_end = __builtin_amdgcn_readfirstlane(off[t.e + 1]);
-  t.row_stop = mt == mt_e - 1 ? row_end : t.row0 + kTileRows;
+  if (BLOCKS) {
+    const int nb = (row_end - row_beg + kTileRowBlock - 1) / kTileRowBlock;
+    t.row0 = row_beg + kTileRowBlock * int(int64_t(mt) * nb / mt_e);
+    t.row_stop = min(row_end, row_beg + kTileRowBlock * int(int64_t(mt + 1) * nb / mt_e));
+  } else {
+    t.row0 = row_beg + mt * kTileRows;
+    t.row_stop = mt == mt_e - 1 ? row_end : t.row0 + kTileRows;
+  }
   return t;
 }
 

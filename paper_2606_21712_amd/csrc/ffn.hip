@@ -21,8 +21,8 @@
 // holds whole chunks.  (Measured against one queue over the whole list, same
 // inputs: GEMM-1 -1% to -4%, GEMM-2 -4% to -7% on the four bf16 workloads.)
 //
-// bf16 tile: 256 rows (an expert's last m-tile up to 320) x 256 weight rows x
-// 64 k per step, 8 wavefronts (2 x 4, two per SIMD so one issues MFMAs while
+// bf16 tile: up to 320 rows of one expert (ceil(rows / 320) m-tiles per expert,
+// cut on 32-row blocks: tiling.h) x 256 weight rows x 64 k per step, 8 wavefronts (2 x 4, two per SIMD so one issues MFMAs while
 // the other waits), each up to 160 x 64: five 32-row blocks of
 // v_mfma_f32_32x32x16_bf16 results, of which a wavefront computes only those
 // holding rows of the tile.  The last round of down-projection tiles, when the
@@ -53,18 +53,17 @@ namespace {
 // Tile counters: GEMM-1's and GEMM-2's queues, then 8 chunk counters of each.
 constexpr int kQueueInts = 18;
 
-// prefix[e] = sum_{e' < e} m-tiles of expert e', prefix[E] = total: ceil(count / bm)
-// m-tiles, or (bm = 256, extra > 0) the count whose last tile takes up to 256 +
-// extra rows.  One block of 256.
+// prefix[e] = sum_{e' < e} m-tiles of expert e', prefix[E] = total, with
+// ceil(count / bm) m-tiles per expert.  One block of 256.
 __global__ __launch_bounds__(256) void tile_prefix_kernel(const int32_t* __restrict__ offsets, int E,
-                                                         int bm, int extra, int32_t* __restrict__ prefix,
+                                                         int bm, int32_t* __restrict__ prefix,
                                                          int32_t* __restrict__ queues) {
   const int e = threadIdx.x;
   if (queues != nullptr && e < kQueueInts) queues[e] = 0;      // tile queues of both GEMMs
   int32_t mt = 0;
   if (e < E) {
     const int32_t c = offsets[e + 1] - offsets[e];
-    mt = extra > 0 ? mtiles_of(c, extra) : (c + bm - 1) / bm;
+    mt = (c + bm - 1) / bm;
   }
   int32_t total;
   const int32_t ex = block_exclusive_scan256(mt, &total);
@@ -73,7 +72,7 @@ __global__ __launch_bounds__(256) void tile_prefix_kernel(const int32_t* __restr
 }
 
 // ----------------------------------------------------------------------------- bf16 MFMA GEMM
-constexpr int kBM = 256;                  // activation rows per m-tile (an expert's last: up to kBMMax)
+constexpr int kBM = 256;                  // m-tile rows of the tile-count bound (ceil(c / 320) <= ceil(c / 256))
 constexpr int kBMMax = kTileRowsMax;      // 320
 constexpr int kBN = 256;                  // weight rows per tile (GEMM-1: 128 gate + 128 up)
 constexpr int kBK = 64;                   // k per pipeline step
@@ -198,7 +197,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
       kt1 = (j + 1) * KT / plan.s;
       slot = q;
     }
-    const TileCoord tc = decode_tile(Lt, s_pref, s_off, p.E, NT);
+    const TileCoord tc = decode_tile<true>(Lt, s_pref, s_off, p.E, NT);
     const int e = tc.e, nt = tc.nt, row0 = tc.row0, row_stop = tc.row_stop;
     const int arows = row_stop - row0;                           // 1 .. 320
 
@@ -467,6 +466,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
 // pieces before adding them (latency, not bandwidth, bounds a strip).
 constexpr int kTailStrips = 16;
 
+template <bool BLOCKS>
 __global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restrict__ partial,
                                                          const int32_t* __restrict__ mtile_prefix,
                                                          const int32_t* __restrict__ offsets, int E, int NT, int G,
@@ -481,7 +481,7 @@ __global__ __launch_bounds__(256) void tail_reduce_kernel(const float* __restric
   const TailPlan plan = tail_plan(int64_t(s_pref[E]) * NT, G, KT);
   const int t = int(blockIdx.x) / kTailStrips;
   if (t >= plan.r) return;                                     // uniform across the block
-  const TileCoord tc = decode_tile(plan.full + t, s_pref, s_off, E, NT);
+  const TileCoord tc = decode_tile<BLOCKS>(plan.full + t, s_pref, s_off, E, NT);
   const int rows = tc.row_stop - tc.row0;
   const int n0 = tc.nt * kTileCols;
   const int cols = min(kTileCols, N - n0);
@@ -617,20 +617,23 @@ int grid_for(int64_t upper_tiles, int num_cu) {
 }  // namespace
 
 hipError_t launch_tail_reduce(const float* partial, const int32_t* mtile_prefix, const int32_t* offsets, int E,
-                              int NT, int G, int KT, int N, uint16_t* y, hipStream_t s) {
+                              int NT, int G, int KT, int N, uint16_t* y, bool row_blocks, hipStream_t s) {
   // A split happens only with at least two pieces of kMinPieceSteps steps; then
   // r <= min(G, kMaxTailPieces) / 2 tail tiles.
   if (KT < 2 * kMinPieceSteps || G < 2) return hipSuccess;
   const int blocks = std::min(G, kMaxTailPieces) / 2 * kTailStrips;
-  MOE_LAUNCH("ffn_tail_reduce", tail_reduce_kernel, dim3(unsigned(blocks)), dim3(256), s, partial, mtile_prefix,
-             offsets, E, NT, G, KT, N, y);
+  if (row_blocks)
+    MOE_LAUNCH("ffn_tail_reduce", tail_reduce_kernel<true>, dim3(unsigned(blocks)), dim3(256), s, partial,
+               mtile_prefix, offsets, E, NT, G, KT, N, y);
+  else
+    MOE_LAUNCH("ffn_tail_reduce", tail_reduce_kernel<false>, dim3(unsigned(blocks)), dim3(256), s, partial,
+               mtile_prefix, offsets, E, NT, G, KT, N, y);
   return hipGetLastError();
 }
 
-hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int extra, int32_t* mtile_prefix,
-                              int32_t* queues, hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, bm, extra, mtile_prefix,
-             queues);
+hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
+                              hipStream_t s) {
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, bm, mtile_prefix, queues);
   return hipGetLastError();
 }
 
@@ -638,8 +641,8 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
                            int64_t R, int E, int H, int F, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues,
                            uint16_t* h, float* partial, int num_cu, hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBM, kTileExtraRows,
-             mtile_prefix, queues);
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kBMMax, mtile_prefix,
+             queues);
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
 
   const int64_t act_bytes = T * H * 2;
@@ -660,7 +663,7 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
   MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_bf16_kernel<false, kRows>), dim3(grid2), dim3(kGemmThreads), s,
              a2);
   const hipError_t err = launch_tail_reduce(partial, mtile_prefix, offsets, E, a2.ntiles, grid2, F / kBK, H,
-                                            y_perm, s);
+                                            y_perm, true, s);
   if (err != hipSuccess) return err;
   return hipGetLastError();
 }
@@ -668,7 +671,7 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
 hipError_t launch_ffn_f32(const float* act, const int32_t* gather, const int32_t* offsets, int64_t R,
                           int E, int H, int F, const float* wg, const float* wu, const float* wd,
                           float* y_perm, int32_t* mtile_prefix, float* h, hipStream_t s) {
-  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, 0, mtile_prefix,
+  MOE_LAUNCH("ffn_tile_prefix", tile_prefix_kernel, dim3(1), dim3(256), s, offsets, E, kFM, mtile_prefix,
              static_cast<int32_t*>(nullptr));
   const int64_t mtiles_upper = (R + int64_t(E) * (kFM - 1)) / kFM;
   GemmArgsF a1{act, gather, wg, wu, h, offsets, mtile_prefix, E, H, F, (F + kFN - 1) / kFN};

@@ -471,7 +471,7 @@ hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* 
                             const uint8_t* wgs, const uint8_t* wu, const uint8_t* wus, const uint8_t* wd,
                             const uint8_t* wds, uint16_t* y_perm, int32_t* mtile_prefix, int32_t* queues, uint8_t* h,
                             uint8_t* hs, float* partial, int num_cu, hipStream_t s) {
-  hipError_t err = launch_tile_prefix(offsets, E, kBM, 0, mtile_prefix, queues, s);
+  hipError_t err = launch_tile_prefix(offsets, E, kBM, mtile_prefix, queues, s);
   if (err != hipSuccess) return err;
   const int64_t mtiles_upper = (R + int64_t(E) * (kBM - 1)) / kBM;
   GemmArgsF8 a1{queues, queues + 2, x, xs, gather, wg, wgs, wu, wus, h, hs, nullptr, nullptr, offsets, mtile_prefix,
@@ -487,7 +487,7 @@ hipError_t launch_ffn_mxfp8(const uint8_t* x, const uint8_t* xs, const int32_t* 
   MOE_LAUNCH("ffn_gemm2_down", (grouped_gemm_fp8_kernel<false, false>), dim3(grid2), dim3(kThreads), s, a2);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  return launch_tail_reduce(partial, mtile_prefix, offsets, E, a2.ntiles, grid2, F / kBK, H, y_perm, s);
+  return launch_tail_reduce(partial, mtile_prefix, offsets, E, a2.ntiles, grid2, F / kBK, H, y_perm, false, s);
 }
 
 }  // namespace moe

@@ -47,13 +47,13 @@ hipError_t launch_ffn_bf16(const uint16_t* act, const int32_t* gather, int64_t T
                            uint16_t* h, float* partial, int num_cu, hipStream_t s);
 // Sums the tail-split pieces of a down projection (G workgroups, KT k steps,
 // NT n-tiles of 256 over N columns) into y; a no-op launch when the plan has none.
+// row_blocks: the GEMM's m-tiles follow the bf16 rule (decode_tile<true>).
 hipError_t launch_tail_reduce(const float* partial, const int32_t* mtile_prefix, const int32_t* offsets, int E,
-                              int NT, int G, int KT, int N, uint16_t* y, hipStream_t s);
-// Per-expert m-tile prefix of the device-side offsets (one block): tiles of bm
-// rows, an expert's last holding up to bm + extra rows; zeroes the GEMMs'
-// tile-queue counters when queues != null.
-hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int extra, int32_t* mtile_prefix,
-                              int32_t* queues, hipStream_t s);
+                              int NT, int G, int KT, int N, uint16_t* y, bool row_blocks, hipStream_t s);
+// Per-expert m-tile prefix of the device-side offsets (one block): ceil(rows /
+// bm) m-tiles per expert; zeroes the GEMMs' tile counters when queues != null.
+hipError_t launch_tile_prefix(const int32_t* offsets, int E, int bm, int32_t* mtile_prefix, int32_t* queues,
+                              hipStream_t s);
 
 // MXFP8: bf16 rows -> E4M3 codes [rows_out, K] + k-step-major E8M0 scales
 // [K / 128][rows_out][4]; output row r reads source row row_map[r] (or r).

@@ -4,15 +4,16 @@
 
 namespace moe {
 
-// Output tiles of the grouped GEMMs are 256 x 256 (GEMM-1: 256 rows x 128
-// features of both gate and up).  An expert's rows are cut into m-tiles of
-// kTileRows; in the bf16 GEMMs the last one may hold up to kTileRows +
-// kTileExtraRows rows, so that a remainder of at most kTileExtraRows rows joins
-// the tile before it instead of costing a tile of its own.
+// Output tiles of the grouped GEMMs are m-tiles of an expert's rows x 256
+// columns (GEMM-1: 128 features of both gate and up).  The bf16 GEMMs cut an
+// expert of c rows into ceil(c / kTileRowsMax) m-tiles whose edges fall on
+// 32-row blocks, the blocks shared out evenly, so every m-tile holds up to
+// kTileRowsMax rows and only the expert's last block is partly filled.  The
+// MXFP8 GEMMs cut it into m-tiles of kTileRows rows, the last one shorter.
 constexpr int kTileRows = 256;
 constexpr int kTileCols = 256;
-constexpr int kTileExtraRows = 64;
-constexpr int kTileRowsMax = kTileRows + kTileExtraRows;
+constexpr int kTileRowsMax = 320;
+constexpr int kTileRowBlock = 32;
 
 // Tail split of the down projection.  A persistent grid of G workgroups runs
 // n output tiles in ceil(n / G) rounds; the last holds only r = n mod G tiles.
