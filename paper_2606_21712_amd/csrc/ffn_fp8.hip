@@ -121,7 +121,9 @@ constexpr int kWScaleOff = 2 * kOpBytes;
 constexpr int kXScaleOff = 2 * kOpBytes + kScaleBytes;
 constexpr int kStageBytes = 2 * kOpBytes + 2 * kScaleBytes;
 constexpr int kThreads = 512;             // 8 wavefronts: 2 (m) x 4 (n)
+constexpr int kEpiBytes = 32 * 144;       // a wavefront's y staging region (32 rows of 128 bytes, padded)
 static_assert(kBM == kTileRows, "tile shape");
+static_assert(8 * kEpiBytes <= kStageBytes, "epilogue staging fits one stage");
 constexpr int kWaitVm0 = 0x0F70;
 constexpr int kBufFlags = 0x00020000;
 
@@ -384,10 +386,17 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
 
-    // ---- epilogue: lane holds columns n + 8 blk + 4 khalf + {0..3} of row (lane % 32)
+    // ---- epilogue: lane holds columns n + 8 blk + 4 khalf + {0..3} of row (lane % 32).
+    // The down projection's y goes through a private LDS region of each wavefront
+    // in st1 (free after the barrier above; the next tile writes it only after its
+    // first barrier): a lane's 8-byte pieces of 32 different rows become whole
+    // 128-byte row segments, 8 rows per store instruction.
+    uint8_t* ebuf = st1 + wave * kEpiBytes;
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) {
-      const int row = row0 + wm * 128 + mi * 32 + rrow;
+      const int rbase = row0 + wm * 128 + mi * 32;             // first row of this 32-row block
+      if (rbase >= row_stop) continue;                          // uniform across the wave
+      const int row = rbase + rrow;
       if (SWIGLU) {
         // the wave's 32 features of this row: one MX block, split between lanes l and l ^ 32
         float hv[16];
@@ -431,20 +440,24 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
             }
           }
         }
-      } else if (row < row_stop) {
-        uint16_t* orow = p.y + int64_t(row) * N;
+      } else if (slot < 0) {
+        // y: 32 rows x 64 columns, rows of 128 bytes in LDS padded to 144
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
+        for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
           for (int blk = 0; blk < 4; ++blk) {
-            const int n = n0 + wn * 64 + ni * 32 + blk * 8 + khalf * 4;
-            if (n < N) {
-              u32x2 pk;
-              pk[0] = pack_bf16x2(acc[mi][ni][blk * 4 + 0], acc[mi][ni][blk * 4 + 1]);
-              pk[1] = pack_bf16x2(acc[mi][ni][blk * 4 + 2], acc[mi][ni][blk * 4 + 3]);
-              *reinterpret_cast<u32x2*>(orow + n) = pk;
-            }
+            u32x2 pk;
+            pk[0] = pack_bf16x2(acc[mi][ni][blk * 4 + 0], acc[mi][ni][blk * 4 + 1]);
+            pk[1] = pack_bf16x2(acc[mi][ni][blk * 4 + 2], acc[mi][ni][blk * 4 + 3]);
+            *reinterpret_cast<u32x2*>(ebuf + rrow * 144 + (ni * 32 + blk * 8 + khalf * 4) * 2) = pk;
           }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = j * 8 + (lane >> 3);
+          const u32x4 v = *reinterpret_cast<const u32x4*>(ebuf + r * 144 + (lane & 7) * 16);
+          const int orow = rbase + r;
+          const int n = n0 + wn * 64 + (lane & 7) * 8;
+          if (orow < row_stop && n < N) *reinterpret_cast<u32x4*>(p.y + int64_t(orow) * N + n) = v;
         }
       }
     }
