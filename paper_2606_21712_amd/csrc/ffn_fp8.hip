@@ -387,10 +387,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
     __syncthreads();
 
     // ---- epilogue: lane holds columns n + 8 blk + 4 khalf + {0..3} of row (lane % 32).
-    // The down projection's y goes through a private LDS region of each wavefront
-    // in st1 (free after the barrier above; the next tile writes it only after its
-    // first barrier): a lane's 8-byte pieces of 32 different rows become whole
-    // 128-byte row segments, 8 rows per store instruction.
+    // The results go through a private LDS region of each wavefront in st1 (free
+    // after the barrier above; the next tile writes it only after its first
+    // barrier): a lane's pieces of 32 different rows become whole row segments
+    // (h codes: 32 bytes, y: 128 bytes).
     uint8_t* ebuf = st1 + wave * kEpiBytes;
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) {
@@ -408,21 +408,24 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
         }
         amax = fmaxf(amax, __shfl_xor(amax, 32));
         const int f0 = n0 + wn * 32;                           // block start, a multiple of 32
-        if (row < row_stop && f0 < N) {
-          const int se = mx_shared_exp(amax);
-          const float inv = mx_inv_scale(se);
-          uint8_t* crow = p.h_codes + int64_t(row) * N + f0 + khalf * 4;
+        const int se = mx_shared_exp(amax);
+        const float inv = mx_inv_scale(se);
+        // the codes of the 32 rows x 32 features go through the wavefront's LDS
+        // region (rows of 48 bytes) and leave as 16-byte pieces of whole rows
 #pragma unroll
-          for (int blk = 0; blk < 4; ++blk) {
-            const float* hb = hv + blk * 4;
-            *reinterpret_cast<uint32_t*>(crow + blk * 8) =
-                e4m3_pack4(hb[0] * inv, hb[1] * inv, hb[2] * inv, hb[3] * inv);
-          }
-          if (khalf == 0) {
-            const int b = f0 / 32;
-            p.h_scales[(int64_t(b / 4) * p.R + row) * 4 + (b & 3)] = uint8_t(se + 127);
-          }
+        for (int blk = 0; blk < 4; ++blk) {
+          const float* hb = hv + blk * 4;
+          *reinterpret_cast<uint32_t*>(ebuf + rrow * 48 + blk * 8 + khalf * 4) =
+              e4m3_pack4(hb[0] * inv, hb[1] * inv, hb[2] * inv, hb[3] * inv);
         }
+        if (row < row_stop && f0 < N && khalf == 0) {
+          const int b = f0 / 32;
+          p.h_scales[(int64_t(b / 4) * p.R + row) * 4 + (b & 3)] = uint8_t(se + 127);
+        }
+        const int r = lane >> 1, ch = lane & 1;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(ebuf + r * 48 + ch * 16);
+        if (rbase + r < row_stop && f0 < N)
+          *reinterpret_cast<u32x4*>(p.h_codes + int64_t(rbase + r) * N + f0 + ch * 16) = v;
       } else if (row < row_stop && slot >= 0) {
         // a piece of a tail tile: fp32 partial sums in its slot, tile-local
         // [256 rows][256 columns], added in piece order by the tail reduction
