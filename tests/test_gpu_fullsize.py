@@ -4,9 +4,10 @@ Routing and permutation are compared bit-exactly on every token.  The FFN and
 the layer output are compared on samples the oracle computes row by row: for
 every expert group its first, middle and last rows of y_perm (so the 1-, 17- and
 31-row groups of the memory-constrained workload are all covered) and one random
-row of every 256-row m-tile of the group (each row in full, so every n-tile of
-every m-tile is checked), and the final y of a token sample that touches every
-expert.  Bars as in test_gpu_parity."""
+row of every 64-row window of the group, each row in full, so every n-tile of
+every m-tile is checked: an expert of more than one m-tile has m-tiles of 160 to
+320 rows, each holding at least one whole window.  Then the final y of a token sample that touches every expert.
+Bars as in test_gpu_parity."""
 import numpy as np
 import pytest
 import torch
@@ -64,8 +65,8 @@ def test_full_size_layer(name):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
         if hi > lo:
             pick = {lo, (lo + hi) // 2, hi - 1}
-            for m0 in range(lo, hi, 256):
-                pick.add(int(rng_rows.integers(m0, min(hi, m0 + 256))))
+            for m0 in range(lo, hi, 64):
+                pick.add(int(rng_rows.integers(m0, min(hi, m0 + 64))))
             rows += sorted(pick)
     rows = np.array(rows)
     xp = to_host(layer.perm["x_perm"][torch.from_numpy(rows).cuda()])

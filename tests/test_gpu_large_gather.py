@@ -6,7 +6,7 @@ x; from 2 GiB on, the loads take 64-bit per-lane row addresses.  Here x is
 2.18 GB (266240 tokens x 4096 hidden, bf16), so the rows of the last ~5900
 tokens start beyond byte 2^31.  Routing and grouping are bit-exact on every
 token; y_perm equals the x_perm path bit for bit; the oracle checks one random
-row of every 256-row m-tile of every expert group and the rows of the last
+row of every 64-row window of every expert group (every m-tile holds one) and the rows of the last
 tokens, each in full, against the bar of the bf16 layer."""
 import numpy as np
 import pytest
@@ -49,8 +49,8 @@ def test_gather_beyond_2gib():
     rows = set()
     for e in range(E):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
-        for m0 in range(lo, hi, 256):
-            rows.add(int(rng.integers(m0, min(hi, m0 + 256))))
+        for m0 in range(lo, hi, 64):                          # every m-tile holds a whole window
+            rows.add(int(rng.integers(m0, min(hi, m0 + 64))))
     far = np.nonzero(stok >= T - 64)[0]                 # rows of the last tokens: offsets past 2^31
     rows.update(far.tolist())
     rows = np.array(sorted(rows))
