@@ -4,7 +4,9 @@ gathering their codes; the down projection's tail split at the device's grid).
 
 Routing and grouping are compared bit-exactly on every token.  The rest is
 checked on samples the oracle computes directly from the format: for every
-expert group its first, middle and last rows, on which
+expert group its first, middle and last rows and one random row of each of its
+256-row m-tiles (the MXFP8 GEMMs cut an expert's rows into m-tiles of 256 from
+its first row), on which
   * the x codes and scales of the row's token equal the oracle's quantization;
   * four 32-feature blocks of the kernel's h are a valid MXFP8 quantization of
     the exact h (from the oracle's x and weight codes) within the accumulation
@@ -109,7 +111,9 @@ def test_full_size_layer_mxfp8(name):
     for e in range(E):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
         if hi > lo:
-            for r in sorted({lo, (lo + hi) // 2, hi - 1}):
+            pick = {lo, (lo + hi) // 2, hi - 1}
+            pick.update(int(rng.integers(m0, min(hi, m0 + 256))) for m0 in range(lo, hi, 256))
+            for r in sorted(pick):
                 rows.append(r)
                 e_of.append(e)
     rows = np.array(rows)
