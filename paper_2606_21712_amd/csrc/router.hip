@@ -5,14 +5,16 @@
 // ties to the lower expert id, softmax over the selected (or all) logits.  The
 // logits never leave the chip unless the caller asks for them.
 //
-// One wavefront takes MB blocks of 16 tokens against all experts (E <= 64: up to
-// four 16-expert blocks of v_mfma_f32_16x16x32_bf16), streaming its token rows
-// once; the router matrix (at most 64 x H bf16) stays in L2 and is read once per
-// wavefront, so larger MB (chosen when there are enough tokens to fill the GPU)
-// reads it less often.  Loads run four k-steps of 32 ahead.  The fp32 logits go
-// through LDS to the selection, where 4 lanes hold one token's logits and each
-// round takes a quad maximum of orderable keys, then a quad minimum of the expert
-// ids holding it (DPP lane permutes).
+// Three kernels, one k order (so a token's result does not depend on its batch):
+// with 64 tokens per compute unit and H % 128 = 0, blocks of four wavefronts share
+// the router matrix through LDS (router_lds_kernel); with fewer tokens and
+// H % 128 = 0, four wavefronts split each 16-token block's k (router_splitk_kernel);
+// otherwise one wavefront takes MB blocks of 16 tokens against all experts
+// (router_kernel), reading the router matrix from L2.  All use
+// v_mfma_f32_16x16x32_bf16 on up to four 16-expert blocks (E <= 64).  The fp32
+// logits go through LDS to the selection, where 4 lanes hold one token's logits
+// and each round takes a quad maximum of orderable keys, then a quad minimum of
+// the expert ids holding it (DPP lane permutes).
 #include "common.h"
 #include "moe_internal.h"
 
@@ -218,18 +220,17 @@ __global__ __launch_bounds__(64) void router_kernel(const uint16_t* __restrict__
 }
 
 // Large batches: four wavefronts per block (64 tokens), the router matrix staged
-// through LDS in k-slices of 256 that the four share, so L2 serves it once per
-// block instead of once per wavefront.  Slices are double-buffered and filled by
-// direct global -> LDS loads; the 16-byte chunks of each 512-byte expert row are
-// stored at chunk ^ (row & 15), so the 16 expert rows an MFMA operand read
+// through LDS in k-slices of SK (256 or 128) that the four share, so L2 serves it
+// once per block instead of once per wavefront.  Slices are double-buffered and
+// filled by direct global -> LDS loads; the 16-byte chunks of each 2 SK-byte expert
+// row are stored at chunk ^ (row & 15), so the 16 expert rows an MFMA operand read
 // touches land on distinct banks.  Each wavefront streams its 16 token rows into
-// registers one slice ahead.  Selection as in router_kernel.
+// registers one slice ahead.  The logits for the selection reuse the slices' LDS
+// once the k loop is done, which keeps a block at 2 SK x E bytes (64 KB at E = 64,
+// SK = 256: two blocks per compute unit).  Selection as in router_kernel.
 constexpr int kLdsWaves = 4;
-constexpr int kSliceK = 256;                          // k per slice
-constexpr int kSliceRowBytes = kSliceK * 2;           // 512
-constexpr int kSliceSteps = kSliceK / 32;             // MFMA k-steps per slice
 
-template <int NB, int KMAX>
+template <int NB, int KMAX, int SK>
 __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16_t* __restrict__ x,
                                                                    const uint16_t* __restrict__ w, int64_t T,
                                                                    int E, int k, int H, int renormalize,
@@ -238,10 +239,17 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
                                                                    float* __restrict__ topk_w) {
   constexpr int EP = 16 * NB;
   constexpr int V = EP / 4;
-  constexpr int kSliceBytes = EP * kSliceRowBytes;    // NB * 8 KB
-  __shared__ __attribute__((aligned(1024))) uint8_t ws0[kSliceBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t ws1[kSliceBytes];
-  __shared__ float s_log[kLdsWaves][kTok][EP + 1];
+  constexpr int kSliceRowBytes = SK * 2;              // one expert row of a slice
+  constexpr int kSliceSteps = SK / 32;                // MFMA k-steps per slice
+  constexpr int kRowsPerDma = 1024 / kSliceRowBytes;  // expert rows per 1 KB load
+  constexpr int kRowChunks = kSliceRowBytes / 16;     // 16-byte chunks per row
+  constexpr int kSliceBytes = EP * kSliceRowBytes;
+  // two slices; after the k loop the same bytes hold the wavefronts' logits
+  __shared__ __attribute__((aligned(1024))) uint8_t ws[2 * kSliceBytes];
+  static_assert(sizeof(float) * kLdsWaves * kTok * (EP + 1) <= 2 * kSliceBytes, "logits fit the slices");
+  uint8_t* const ws0 = ws;
+  uint8_t* const ws1 = ws + kSliceBytes;
+  float (*s_log)[kTok][EP + 1] = reinterpret_cast<float (*)[kTok][EP + 1]>(ws);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -257,11 +265,12 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
   const bf16x8* xr = reinterpret_cast<const bf16x8*>(x + (xv ? t0 + r16 : 0) * H + kq * 8);
   const bf16x8 zero = {};
 
-  // slice DMA: NB * 8 instructions of 1 KB (two 512-byte expert rows each), dealt
-  // over the four wavefronts; lane q fills row 2 i + q / 32, chunk position q % 32
+  // slice DMA: 1 KB instructions of kRowsPerDma expert rows each, dealt over the
+  // four wavefronts; lane q fills row kRowsPerDma i + q / kRowChunks, chunk position
+  // q % kRowChunks
   const __amdgpu_buffer_rsrc_t rw =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w), 0, int(int64_t(E) * H * 2), 0x00020000);
-  constexpr int kDma = NB * 8;
+  constexpr int kDma = EP / kRowsPerDma;
   constexpr int kDmaPerWave = (kDma + kLdsWaves - 1) / kLdsWaves;
   // (a fixed-size array: sized by the template-dependent count, the host pass
   // drops the kernel's launch stub)
@@ -270,8 +279,8 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) {
     const int i = j * kLdsWaves + wave;               // instruction index
-    const int row = 2 * i + (lane >> 5);
-    const int pos = lane & 31;
+    const int row = kRowsPerDma * i + lane / kRowChunks;
+    const int pos = lane % kRowChunks;
     const int chunk = pos ^ (row & 15);               // logical 16-byte chunk this lane fetches
     woff[j] = row < E ? uint32_t(row) * uint32_t(H) * 2u + uint32_t(chunk) * 16u : 0x80000000u;
   }
@@ -286,7 +295,7 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
   auto load_x = [&](bf16x8* a, int s) {
 #pragma unroll
     for (int u = 0; u < kSliceSteps; ++u)
-      a[u] = xv ? __builtin_nontemporal_load(xr + (s * kSliceK + 32 * u) / 8) : zero;
+      a[u] = xv ? __builtin_nontemporal_load(xr + (s * SK + 32 * u) / 8) : zero;
   };
 
   f32x4 acc[NB], tot[NB];
@@ -315,7 +324,7 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
     }
   };
 
-  const int S = H / kSliceK;
+  const int S = H / SK;
   bf16x8 xa[2][kSliceSteps];
   issue_w(ws0, 0);
   load_x(xa[0], 0);
@@ -336,6 +345,7 @@ __global__ __launch_bounds__(kLdsWaves * 64) void router_lds_kernel(const uint16
   if (s < S) step(ws0, ws1, xa[0], xa[1], s);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = tot[nb] + acc[nb];   // the last quarter
+  __syncthreads();                                    // every wave is done with the slices
 
   // 16 x 16 outputs: lane holds tokens 4 (lane / 16) + q of expert column lane % 16
 #pragma unroll
@@ -572,19 +582,19 @@ hipError_t launch_splitk(const uint16_t* x, const uint16_t* w, int64_t T, int E,
   return hipGetLastError();
 }
 
-template <int NB>
+template <int NB, int SK>
 hipError_t launch_lds(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
                       float* logits, int32_t* ids, float* wts, hipStream_t s) {
   const dim3 grid(unsigned((T + kLdsWaves * kTok - 1) / (kLdsWaves * kTok)));
   const dim3 block(kLdsWaves * 64);
   if (k <= 4)
-    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, 4>), grid, block, s, x, w, T, E, k, H, renorm, logits, ids,
+    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, 4, SK>), grid, block, s, x, w, T, E, k, H, renorm, logits, ids,
                wts);
   else if (k <= 8)
-    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, 8>), grid, block, s, x, w, T, E, k, H, renorm, logits, ids,
+    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, 8, SK>), grid, block, s, x, w, T, E, k, H, renorm, logits, ids,
                wts);
   else
-    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, kMaxTopK>), grid, block, s, x, w, T, E, k, H, renorm, logits,
+    MOE_LAUNCH("router_topk", (router_lds_kernel<NB, kMaxTopK, SK>), grid, block, s, x, w, T, E, k, H, renorm, logits,
                ids, wts);
   return hipGetLastError();
 }
@@ -611,8 +621,11 @@ template <int NB>
 hipError_t launch_nb(const uint16_t* x, const uint16_t* w, int64_t T, int E, int k, int H, int renorm,
                      float* logits, int32_t* ids, float* wts, int num_cu, hipStream_t s) {
   // Enough 64-token blocks for every compute unit: the LDS-staged kernel.
-  if (H % kSliceK == 0 && T >= int64_t(num_cu) * kLdsWaves * kTok)
-    return launch_lds<NB>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
+  // Slices of 256 k where H allows (half the barriers of 128), else of 128.
+  if (H % 128 == 0 && T >= int64_t(num_cu) * kLdsWaves * kTok) {
+    if (H % 256 == 0) return launch_lds<NB, 256>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
+    return launch_lds<NB, 128>(x, w, T, E, k, H, renorm, logits, ids, wts, s);
+  }
   const int64_t waves_wanted = int64_t(num_cu) * 8;
   // Fewer than 8 sixteen-token wavefronts per compute unit: split k four ways.
   if (H % (kSplitWaves * 32) == 0 && T < waves_wanted * kTok)

@@ -52,15 +52,16 @@ def check(x, w, k, renorm=1, exact_ties=False):
     return safe.mean()
 
 
-# With H % 256 != 0 (or fewer than 64 tokens per compute unit) the per-wavefront
-# kernel runs: T >= 65536 and >= 131072 give a wavefront 32 and 64 tokens (on 256
-# compute units).  H % 256 == 0 with T >= 16384 runs the LDS-staged kernel: 1 to 4
-# expert blocks, 4, 8 and 16 selection slots, ragged last block of 64 tokens.
+# With H % 128 != 0 the per-wavefront kernel runs: T >= 65536 and >= 131072 give a
+# wavefront 32 and 64 tokens (on 256 compute units).  H % 128 == 0 with T >= 16384
+# runs the LDS-staged kernel (k-slices of 256 where H % 256 == 0, else of 128): 1
+# to 4 expert blocks, 4, 8 and 16 selection slots, ragged last block of 64 tokens;
+# below 16384 tokens the split-k kernel.
 @pytest.mark.parametrize("T,E,k,H", [(1000, 8, 2, 256), (333, 64, 8, 448), (77, 3, 3, 64), (500, 40, 6, 4096),
                                      (129, 16, 4, 192), (257, 33, 16, 320), (5, 64, 1, 128),
-                                     (70001, 20, 3, 64), (140007, 64, 4, 128),
+                                     (70001, 20, 3, 64), (140007, 64, 4, 192), (40003, 64, 4, 128),
                                      (16384, 8, 2, 768), (20000, 64, 8, 256), (17000, 40, 4, 512),
-                                     (33333, 20, 16, 1024)])
+                                     (33333, 20, 16, 1024), (20011, 48, 8, 384), (16391, 61, 8, 1152)])
 def test_router_random(T, E, k, H):
     rng = np.random.default_rng(T + E + H)
     x = moegen.round_bf16(rng.standard_normal((T, H)).astype(np.float32))
@@ -101,9 +102,10 @@ def test_router_batch_size_invariant(H, sizes):
     logits, ids and weights: every kernel variant (k split four ways for small
     batches, LDS-staged router matrix, 16 / 32 / 64 tokens per wavefront) adds the
     products in the same k order.  A budget of 4 compute units puts the variants'
-    switch points at small T: with H = 640 the sizes run split-k, then 16, 32 and 64
-    tokens per wavefront; with H = 1024 split-k, then the LDS-staged kernel; H = 192
-    (H % 128 != 0) runs one k chain in every per-wavefront variant."""
+    switch points at small T: with H = 640 the sizes run split-k, then the
+    LDS-staged kernel with k-slices of 128; with H = 1024 split-k, then the
+    LDS-staged kernel with slices of 256; H = 192 (H % 128 != 0) runs one k chain in
+    the per-wavefront kernel at 16, 16, 32 and 64 tokens per wavefront."""
     rng = np.random.default_rng(H)
     E, k = 64, 4
     x = moegen.round_bf16(rng.standard_normal((max(sizes), H)).astype(np.float32))
