@@ -1143,6 +1143,63 @@ def summarize_probe(root):
     print("\n".join(lines))
 
 
+def summarize_dense(root):
+    """Counters of the GEMM dispatches of a --dense-ceiling run (the vendor library's
+    kernels beside this library's grouped ones) from the --pmc passes under root.
+    Per kernel name, the dispatches within 80% of its longest (for the vendor kernel:
+    the one dense GEMM of the projection's whole size, not the per-expert ones);
+    medians over them."""
+    import glob
+    import re
+    per = {}
+    for path in sorted(glob.glob(os.path.join(root, "*", "*counter_collection.csv"))):
+        by_disp = {}
+        for r in _read_csv(path):
+            n = r["Kernel_Name"]
+            if "Cijk" not in n and "grouped_gemm" not in n:
+                continue
+            d = by_disp.setdefault(int(r["Dispatch_Id"]), dict(name=n, counters={}))
+            d["counters"][r["Counter_Name"]] = d["counters"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            d["us"] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        longest = {}
+        for d in by_disp.values():
+            longest[d["name"]] = max(longest.get(d["name"], 0.0), d["us"])
+        for d in by_disp.values():
+            if d["us"] < 0.8 * longest[d["name"]]:
+                continue
+            m = re.search(r"MT\d+x\d+x\d+", d["name"])
+            k = re.search(r"(\w+_kernel<[^()]*>)", d["name"])
+            label = f"hipBLASLt {m.group(0)}" if m else (k.group(1) if k else d["name"][:60])
+            slot = per.setdefault(label, {})
+            for k, v in d["counters"].items():
+                slot.setdefault(k, []).append(v)
+            slot.setdefault("us", []).append(d["us"])
+    lines = ["| kernel | dispatches | us (pmc run) | clock GHz | MFMA busy % | MFMA flop (counted) | "
+             "L1->L2 read requests | mean L1->L2 latency, cycles | L1 pending-miss stall % | L2 hit % |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for name, sl in sorted(per.items(), key=lambda kv: -float(np.median(kv[1]["us"]))):
+        m = {k: float(np.median(v)) for k, v in sl.items()}
+        cyc = m.get("GRBM_GUI_ACTIVE", 0) / NUM_XCD
+
+        def f(v, fmt):
+            return "-" if v is None else format(v, fmt)
+        # the GRBM window includes the dispatch itself: the clock is meaningful for long kernels only
+        clk = cyc / (m["us"] * 1e3) if cyc and m["us"] >= 100 else None
+        busy = 100 * m["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * NUM_SIMD) if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in m \
+            else None
+        mops = sum(m.get(k, 0.0) for k in ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F8",
+                                            "SQ_INSTS_VALU_MFMA_MOPS_F6F4"))
+        req = m.get("TCP_TCC_READ_REQ")
+        lat = m["TCP_TCC_READ_REQ_LATENCY"] / req if req and "TCP_TCC_READ_REQ_LATENCY" in m else None
+        pend = 100 * m["TCP_PENDING_STALL_CYCLES"] / (cyc * NUM_CU) if cyc and "TCP_PENDING_STALL_CYCLES" in m \
+            else None
+        hit = 100 * m["TCC_HIT"] / (m["TCC_HIT"] + m["TCC_MISS"]) if "TCC_HIT" in m and "TCC_MISS" in m else None
+        lines.append(f"| `{name}` | {len(sl['us'])} | {m['us']:.1f} | {f(clk, '.3f')} | {f(busy, '.1f')} | "
+                     f"{f(mops * 512 if mops else None, '.3e')} | {f(req, '.3e')} | {f(lat, '.0f')} | "
+                     f"{f(pend, '.1f')} | {f(hit, '.1f')} |")
+    print("\n".join(lines))
+
+
 def main():
     import moegen
 
@@ -1163,6 +1220,8 @@ def main():
                          "counter passes of --profile-run / default runs of --config)")
     ap.add_argument("--probe", action="store_true",
                     help="with --summarize: counters per kernel instantiation of a --route-probe run")
+    ap.add_argument("--dense", action="store_true",
+                    help="with --summarize: counters of the GEMMs of a --dense-ceiling run")
     ap.add_argument("--mfma-ceiling", action="store_true",
                     help="the matrix cores' rate with no memory traffic (register-only probe), bf16 and fp8")
     ap.add_argument("--dense-ceiling", action="store_true",
@@ -1180,6 +1239,8 @@ def main():
     args = ap.parse_args()
     if args.summarize and args.probe:
         return summarize_probe(args.summarize)
+    if args.summarize and args.dense:
+        return summarize_dense(args.summarize)
     if args.summarize:
         return summarize(args.summarize, moegen.CONFIGS[args.config], args.warmup, args.steps,
                          gather=not args.no_gather, mx=args.mxfp8)
