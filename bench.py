@@ -650,6 +650,62 @@ def fit_ffn_model(rows, weight_bytes: float):
                 max_abs_residual_pct=round(100 * float(np.max(np.abs(pred / t - 1.0))), 2))
 
 
+def graph_probe(steps: int, warmup: int):
+    """Small expert batches, where launches rather than the kernels set the pace: one
+    layer step issued call by call (eager: the Python binding's calls, each a kernel
+    launch or two) against the same step captured once as a HIP graph (LayerGraph)
+    and replayed, T = 256 .. 4096 tokens on the Mixtral and DeepSeek shapes (router
+    logits, gather path).  Per size: ms per step back to back over `steps` steps,
+    both ways, and the sum of the kernels' own times (the library's profiler, eager
+    steps).  One JSON line per size."""
+    import torch
+
+    import moegen
+    import paper_2606_21712_amd as moe
+
+    for name in ("mixtral4k", "deepseek"):
+        base = moegen.CONFIGS[name]
+        cfg = base.scaled(T=4096)
+        log(f"graph probe {name}: generating T={cfg.T} H={cfg.H} E={cfg.E} k={cfg.k} F={cfg.F} Fs={cfg.Fs}")
+        I = moegen.make_inputs(cfg)
+        x_all, l_all = to_dev(I.x, torch), to_dev(I.logits, torch)
+        W = [to_dev(a, torch) for a in (I.w_gate, I.w_up, I.w_down)]
+        W += [to_dev(a, torch) for a in (I.ws_gate, I.ws_up, I.ws_down)] if cfg.Fs else [None, None, None]
+        T = 256
+        while T <= cfg.T:
+            layer = moe.MoELayer(T, cfg.H, cfg.E, cfg.k, cfg.F, cfg.Fs, gather=True)
+            x, lg = x_all[:T].contiguous(), l_all[:T].contiguous()
+
+            def eager():
+                layer.run(x, lg, *W, renormalize=cfg.renormalize)
+
+            g = moe.LayerGraph(layer, x, lg, *W, renormalize=cfg.renormalize)
+            out = {}
+            for mode, fn in (("eager", eager), ("graph", g.replay)):
+                for _ in range(warmup):
+                    fn()
+                torch.cuda.synchronize()
+                ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ev0.record()
+                for _ in range(steps):
+                    fn()
+                ev1.record()
+                torch.cuda.synchronize()
+                out[mode] = ev0.elapsed_time(ev1) / steps
+            moe.profiler_start(steps * 16 + 16)
+            for _ in range(steps):
+                eager()
+            torch.cuda.synchronize()
+            moe.profiler_stop()
+            kern = sum(t for _, t in moe.profiler_records()) / steps
+            print(json.dumps({"graph_probe": name, "tokens": T, "eager_ms": round(out["eager"], 4),
+                              "graph_ms": round(out["graph"], 4), "kernels_ms": round(kern, 4),
+                              "speedup": round(out["eager"] / out["graph"], 3),
+                              "graph_tokens_per_s": round(T / out["graph"] * 1e3, 1)}), flush=True)
+            del g, layer
+            T *= 2
+
+
 def expert_batch_sweep(shape: str, steps: int, warmup: int):
     """Module-level roofline of the MoE layer: time one layer over expert batches of
     T = 256 .. T_max tokens and report tokens/s and grouped-FFN TFLOP/s per size,
@@ -1234,6 +1290,8 @@ def main():
                     help="time the layer with MXFP8 expert GEMMs on --config (a separate JSON line)")
     ap.add_argument("--router-probe", action="store_true",
                     help="only time moe_router_topk (router GEMM + gate) on the layer shapes")
+    ap.add_argument("--graph-probe", action="store_true",
+                    help="small batches: a layer step call by call against the same step replayed as a HIP graph")
     ap.add_argument("--route-probe", action="store_true",
                     help="only time moe_route at 2^20 tokens (bandwidth probe), cold and warm")
     args = ap.parse_args()
@@ -1252,6 +1310,8 @@ def main():
         return mfma_ceiling()
     if args.route_probe:
         return route_probe()
+    if args.graph_probe:
+        return graph_probe(args.steps, args.warmup)
     if args.router_probe:
         return router_probe()
     if args.mxfp8:

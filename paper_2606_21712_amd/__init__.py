@@ -21,7 +21,7 @@ __all__ = [
     "moe_permute_workspace_bytes", "moe_grouped_ffn_workspace_bytes", "MoELayer",
     "moe_mxfp8_scale_bytes", "moe_quantize_mxfp8", "moe_grouped_ffn_mxfp8_workspace_bytes",
     "moe_grouped_ffn_mxfp8", "moe_grouped_ffn_mxfp8_gather", "MXFP8", "quantize_weights_mxfp8",
-    "MoELayerMXFP8",
+    "MoELayerMXFP8", "LayerGraph",
     "profiler_start", "profiler_select", "profiler_stop", "profiler_records", "set_cu_budget",
     "DTYPE_F32", "DTYPE_BF16",
 ]
@@ -443,6 +443,37 @@ class MoELayer:
         moe_combine(self.y_perm, self.perm["dest_rows"], self.topk_weights, self.y_shared, y=self.y,
                     stream=stream)
         return self.y
+
+
+class LayerGraph:
+    """One layer step captured as a HIP graph: ``replay()`` launches the layer's kernels
+    (route, permute, grouped FFN, combine) as one graph on the current stream, which
+    takes the per-kernel launch cost off small expert batches.
+
+    The graph holds the device addresses of the tensors given at capture and of the
+    layer's own buffers: to run it on new data, copy the data into those tensors in
+    place.  The library's calls neither allocate nor synchronize, and nothing in a
+    layer step clears memory with a memset (the tile counters are zeroed by a kernel),
+    so the whole step captures.  A first eager run on a side stream (of default
+    priority) does the library's one-time set-up outside the capture."""
+
+    def __init__(self, layer, *args, **kwargs):
+        if "stream" in kwargs:
+            raise ValueError("LayerGraph captures on the current stream; pass no stream")
+        self.layer = layer
+        self.graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            layer.run(*args, **kwargs)
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(self.graph):
+            layer.run(*args, **kwargs)
+
+    def replay(self):
+        """Run the captured step on the current stream; returns the layer's y."""
+        self.graph.replay()
+        return self.layer.y
 
 
 class MoELayerMXFP8:

@@ -266,3 +266,11 @@ def test_permute_static_validation(L):
     assert call(T=(1 << 22) // 8 + 128, E=256, k=8) == UNSUPPORTED
     assert b"static" in L.moe_last_error()
     assert call(T=0, ids=None, xp=None) == 0
+
+
+def test_layer_graph_rejects_a_stream():
+    """LayerGraph captures on the current stream; an explicit stream is refused
+    before anything runs."""
+    import paper_2606_21712_amd as moe
+    with pytest.raises(ValueError):
+        moe.LayerGraph(object(), stream=object())
