@@ -77,6 +77,7 @@ struct TileCoord {
   int row0;       // first grouped row of the tile
   int row_stop;   // end of the tile's rows
   int nt;         // n-tile index
+  int mt_e;       // the expert's m-tiles
 };
 
 // Tile L of the list; pref/off are the m-tile prefix and row offsets (E + 1
@@ -101,6 +102,7 @@ __device__ __forceinline__ TileCoord decode_tile(int64_t L, const int32_t* pref,
   const int rem2 = rem - ng * bm * kGroupN;
   const int mt = mbi * kGroupM + rem2 % bm;
   t.nt = ng * kGroupN + rem2 / bm;
+  t.mt_e = mt_e;
   const int row_beg = __builtin_amdgcn_readfirstlane(off[t.e]);
   const int row_end = __builtin_amdgcn_readfirstlane(off[t.e + 1]);
   if (BLOCKS) {

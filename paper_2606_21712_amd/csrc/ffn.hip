@@ -247,8 +247,20 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
     }
     // The weight passes and the activation passes of a stage's loads.  Activation
     // passes whose 8 rows all lie past the tile are not issued.
+    // k-step order.  A down-projection tile of an expert that has a single m-tile
+    // shares its weight panel with no other tile, and with rows of at most 8 KB the
+    // same k column of every weight row lands on the same HBM channels, so the
+    // tiles running at one time would all ask the same channels at each step:
+    // such a tile starts its k loop at a step of its own and wraps around.  (Tiles
+    // that share panels keep one order, so the L2 sees their reads together.)
+    const int nk = kt1 - kt0;
+    const int krot = (!SWIGLU && slot < 0 && tc.mt_e == 1 && K * 2 <= 8192) ? int((Lt * 7) % nk) : 0;
+    auto kphys = [&](int kt) {
+      const int q = kt - kt0 + krot;
+      return kt0 + (q >= nk ? q - nk : q);
+    };
     auto issue_w = [&](uint8_t* stage, int kt) {
-      const int kb = kt * kRowBytes;
+      const int kb = kphys(kt) * kRowBytes;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int blk = 8 * i + wave;
@@ -257,7 +269,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_bf16_kernel(Gemm
       }
     };
     auto issue_a = [&](uint8_t* stage, int kt) {
-      const int kb = kt * kRowBytes;
+      const int kb = kphys(kt) * kRowBytes;
 #pragma unroll
       for (int i = 0; i < 5; ++i) {
         const int blk = 8 * i + wave;
