@@ -47,15 +47,15 @@ CPU_SAMPLE = {"tiny": 256, "mixtral4k": 4096, "mixtral32k_zipf": 4096, "deepseek
               "memconstrained": 4096}
 
 
-def gemm_source_sha256() -> str:
-    """sha256 of the grouped-GEMM source (ffn.hip, then the common.h it includes)
-    with comments removed and whitespace collapsed, so that only code changes
-    invalidate counters taken on it."""
+def gemm_source_sha256(mx: bool = False) -> str:
+    """sha256 of the grouped-GEMM source (ffn.hip, or ffn_fp8.hip for the MXFP8
+    GEMMs, then the common.h it includes) with comments removed and whitespace
+    collapsed, so that only code changes invalidate counters taken on it."""
     import hashlib
     import re
     csrc = os.path.join(ROOT, "paper_2606_21712_amd", "csrc")
     h = hashlib.sha256()
-    for name in ("ffn.hip", "common.h"):
+    for name in ("ffn_fp8.hip" if mx else "ffn.hip", "common.h"):
         with open(os.path.join(csrc, name)) as f:
             text = f.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)      # block comments
@@ -1150,7 +1150,7 @@ def summarize(root, c, warmup: int, steps: int, gather: bool = True, mx: bool = 
         if g and "FETCH_SIZE" in g and "WRITE_SIZE" in g and factor:
             hbm = float(np.mean(g["FETCH_SIZE"])) * 1024 * factor["FETCH_SIZE"] + \
                 float(np.mean(g["WRITE_SIZE"])) * 1024 * factor["WRITE_SIZE"]
-            lines += [f"source_sha256: {gemm_source_sha256()}", f"gemm1_traffic_bytes_per_launch: {hbm:.6g}", ""]
+            lines += [f"source_sha256: {gemm_source_sha256(mx)}", f"gemm1_traffic_bytes_per_launch: {hbm:.6g}", ""]
     print("\n".join(lines))
 
 
