@@ -267,7 +267,15 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_fp8_kernel(GemmArgsF
 
     // A stage's loads: the activation codes first (gathered rows arrive last),
     // then the weight codes, then the scales.
+    // k-step order: a down-projection tile of an expert with a single m-tile and
+    // rows of at most 8 KB starts at a step of its own (as in the bf16 kernel)
+    const int nk = kt1 - kt0;
+    const int krot = (!SWIGLU && slot < 0 && tc.mt_e == 1 && K <= 8192) ? int((Lt * 7) % nk) : 0;
     auto issue = [&](uint8_t* stage, int kt) {
+      {
+        const int q = kt - kt0 + krot;
+        kt = kt0 + (q >= nk ? q - nk : q);
+      }
       const int kb = kt * kRowBytes;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
