@@ -650,6 +650,50 @@ def fit_ffn_model(rows, weight_bytes: float):
                 max_abs_residual_pct=round(100 * float(np.max(np.abs(pred / t - 1.0))), 2))
 
 
+def stream_probe(reps: int = 7):
+    """How fast 256-row panels stream from HBM one 128-byte k column at a time (the
+    way a grouped-GEMM tile reads its weight panel), against the row pitch K, with
+    every panel starting at column 0 and with panel p starting at column 7 p mod
+    (K / 128): the panel-streaming probe of libmoe_probe.so over 1 GiB of panels,
+    256 persistent workgroups, median of reps launches (HIP events).  One JSON line
+    per (K, order)."""
+    import ctypes
+
+    import torch
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_21712_amd", "libmoe_probe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built (run __graft_entry__.build())")
+    fn = ctypes.CDLL(path).moe_probe_stream_panels
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_void_p]
+    total = 1 << 30
+    w = torch.ones(total, dtype=torch.uint8, device="cuda")
+    ctr = torch.zeros(1, dtype=torch.int32, device="cuda")
+    blocks = 256
+    out = torch.empty(blocks * 512, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for K in (4096, 6144, 7168, 8192, 12288, 14336, 16384, 28672):
+        panels = total // (256 * K)
+        row = {"stream_probe": "panels", "row_bytes": K, "panels": panels}
+        for rot in (0, 1):
+            ts = []
+            for _ in range(reps):
+                ctr.zero_()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                rc = fn(w.data_ptr(), panels, K, rot, blocks, ctr.data_ptr(), out.data_ptr(), stream.cuda_stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                if rc != 0:
+                    raise RuntimeError(f"moe_probe_stream_panels returned {rc}")
+                ts.append(e0.elapsed_time(e1))
+            assert int(ctr.item()) == panels + blocks, "panel counter"
+            ms = float(np.median(ts))
+            row["rotated_TBps" if rot else "column0_TBps"] = round(panels * 256 * K / (ms * 1e-3) / 1e12, 2)
+        print(json.dumps(row), flush=True)
+
+
 def graph_probe(steps: int, warmup: int):
     """Small expert batches, where launches rather than the kernels set the pace: one
     layer step issued call by call (eager: the Python binding's calls, each a kernel
@@ -1290,6 +1334,8 @@ def main():
                     help="time the layer with MXFP8 expert GEMMs on --config (a separate JSON line)")
     ap.add_argument("--router-probe", action="store_true",
                     help="only time moe_router_topk (router GEMM + gate) on the layer shapes")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="weight-panel streaming rate against the row pitch, with and without a per-panel k start")
     ap.add_argument("--graph-probe", action="store_true",
                     help="small batches: a layer step call by call against the same step replayed as a HIP graph")
     ap.add_argument("--route-probe", action="store_true",
@@ -1312,6 +1358,8 @@ def main():
         return route_probe()
     if args.graph_probe:
         return graph_probe(args.steps, args.warmup)
+    if args.stream_probe:
+        return stream_probe()
     if args.router_probe:
         return router_probe()
     if args.mxfp8:

@@ -42,3 +42,40 @@ def test_probe_variants_run():
             torch.cuda.synchronize()
             assert bool(torch.isfinite(out).all()), (fp8, rnd)
             assert float(out.abs().sum()) > 0.0, (fp8, rnd)
+
+
+def _stream():
+    fn = ctypes.CDLL(PATH).moe_probe_stream_panels
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_void_p]
+    return fn
+
+
+def test_stream_probe_rejects_bad_arguments():
+    fn = _stream()
+    p = ctypes.c_void_p(16)
+    assert fn(None, 1, 4096, 0, 1, p, p, None) == 1           # no matrix
+    assert fn(p, 0, 4096, 0, 1, p, p, None) == 1              # no panels
+    assert fn(p, 1, 4000, 0, 1, p, p, None) == 1              # K not a multiple of 128
+    assert fn(p, 1, 1 << 23, 0, 1, p, p, None) == 1           # a panel past 2^31 bytes
+    assert fn(p, 1, 4096, 0, 0, p, p, None) == 1              # no workgroups
+    assert fn(p, 1, 4096, 0, 1, None, p, None) == 1           # no counter
+
+
+@pytest.mark.gpu
+def test_stream_probe_runs():
+    """Both orders run to completion: every panel claimed once, then one failed
+    claim per workgroup."""
+    import torch
+    fn = _stream()
+    K, panels, blocks = 4096, 24, 16
+    w = torch.ones(panels * 256 * K, dtype=torch.uint8, device="cuda")
+    ctr = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = torch.empty(blocks * 512, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    for rot in (0, 1):
+        ctr.zero_()
+        assert fn(w.data_ptr(), panels, K, rot, blocks, ctr.data_ptr(), out.data_ptr(), stream) == 0
+        torch.cuda.synchronize()
+        assert int(ctr.item()) == panels + blocks
