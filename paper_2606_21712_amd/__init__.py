@@ -461,6 +461,8 @@ class LayerGraph:
         if "stream" in kwargs:
             raise ValueError("LayerGraph captures on the current stream; pass no stream")
         self.layer = layer
+        # the graph reads these tensors by address: keep them alive as long as it is
+        self._captured = (args, kwargs)
         self.graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
