@@ -692,6 +692,24 @@ def stream_probe(reps: int = 7):
             ms = float(np.median(ts))
             row["rotated_TBps" if rot else "column0_TBps"] = round(panels * 256 * K / (ms * 1e-3) / 1e12, 2)
         print(json.dumps(row), flush=True)
+    # the other direction: 16-byte nontemporal stores alone over the same 1 GiB
+    wfn = ctypes.CDLL(path).moe_probe_write
+    wfn.restype = ctypes.c_int
+    wfn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p]
+    for wblocks in (2048, 8192):
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = wfn(w.data_ptr(), total, wblocks, stream.cuda_stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if rc != 0:
+                raise RuntimeError(f"moe_probe_write returned {rc}")
+            ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        print(json.dumps({"stream_probe": "write", "bytes": total, "blocks": wblocks,
+                          "TBps": round(total / (ms * 1e-3) / 1e12, 2)}), flush=True)
 
 
 def graph_probe(steps: int, warmup: int):

@@ -79,3 +79,26 @@ def test_stream_probe_runs():
         assert fn(w.data_ptr(), panels, K, rot, blocks, ctr.data_ptr(), out.data_ptr(), stream) == 0
         torch.cuda.synchronize()
         assert int(ctr.item()) == panels + blocks
+
+
+def test_write_probe_rejects_bad_arguments():
+    fn = ctypes.CDLL(PATH).moe_probe_write
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p]
+    p = ctypes.c_void_p(16)
+    assert fn(None, 1024, 1, None) == 1                       # no buffer
+    assert fn(p, 1000, 1, None) == 1                          # not a multiple of 16
+    assert fn(p, 1024, 0, None) == 1                          # no workgroups
+
+
+@pytest.mark.gpu
+def test_write_probe_fills_the_buffer():
+    import torch
+    fn = ctypes.CDLL(PATH).moe_probe_write
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p]
+    buf = torch.full((1 << 20,), -1, dtype=torch.int32, device="cuda")
+    assert fn(buf.data_ptr(), buf.numel() * 4, 64, torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    v = buf.view(-1, 4).cpu()
+    assert bool((v[:, 2] == 0).all()) and bool((v[:, 3] == 0).all())   # every 16-byte slot written
