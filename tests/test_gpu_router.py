@@ -34,6 +34,12 @@ def run(x, w, k, renorm=1):
 
 def check(x, w, k, renorm=1, exact_ties=False):
     lg, ids, wt = run(x, w, k, renorm)
+    return check_outputs(x, w, k, renorm, lg, ids, wt, exact_ties)
+
+
+def check_outputs(x, w, k, renorm, lg, ids, wt, exact_ties=False):
+    """The kernel's logits, ids and weights for the token rows x (all of them, or a
+    sample: each token is checked on its own) against the oracle."""
     exact = oracle.router_logits(x, w)
     bound = ACC * (np.abs(oracle.moe_oracle._f64(x)) @ np.abs(oracle.moe_oracle._f64(w)).T) + 1e-30
     assert (np.abs(lg.astype(np.float64) - exact) <= bound).all()
@@ -126,3 +132,19 @@ def test_router_batch_size_invariant(H, sizes):
                                           b.view(np.uint32) if b.dtype == np.float32 else b), (H, T)
     finally:
         moe.set_cu_budget(0)
+
+
+def test_router_fullsize_memconstrained():
+    """The memory-constrained workload's router at full size (131072 tokens, H 4096,
+    64 experts, top-4: the LDS-staged kernel with k-slices of 256 on every compute
+    unit), checked on 4096 sampled tokens and the last 64 (the ragged end)."""
+    I = moegen.make_inputs("memconstrained", with_weights=False)
+    c = I.cfg
+    w = I.extra["w_router"]
+    log(f"[gpu] router full size memconstrained T={c.T} H={c.H} E={c.E} k={c.k}")
+    lg, ids, wt = run(I.x, w, c.k)
+    rng = np.random.default_rng(7)
+    rows = np.unique(np.concatenate([rng.choice(c.T, 4096, replace=False), np.arange(c.T - 64, c.T)]))
+    frac = check_outputs(I.x[rows], w, c.k, 1, lg[rows], ids[rows], wt[rows])
+    log(f"[gpu]   {frac:.4f} of the sampled tokens checked against the exact logits' routing")
+    assert frac > 0.9
